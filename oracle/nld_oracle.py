@@ -1,0 +1,374 @@
+"""CPU oracle for one block-decode step of linear self-speculation.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only the test suite, the package smoke check and the
+CPU-baseline leg of the benchmark use it.  It shares no code with the GPU
+path; the two meet only in the seeded input generator (``synth``).
+
+What it computes (arXiv 2607.05722):
+
+* Linear self-speculation, Sec. 3.3 ("Mode 3: Self-Speculation Decoding"):
+  a diffusion *draft* pass over a block that holds mask tokens after the
+  verified prefix, then an AR *verify* pass over the draft tokens with causal
+  attention that reuses the prefix KV cache, then acceptance of the longest
+  draft prefix that matches the AR predictions plus one token from the AR
+  prediction at the first rejected position.
+* The attention pattern follows Sec. 2.1 (block-wise diffusion objective:
+  bidirectional within a block, causal across blocks) and Sec. 2.2 (the clean
+  stream is strictly causal).
+* Mode 1 (Sec. 3.1), AR decoding, is the verify pass with a one-token block.
+* The first-mismatch index j* of the LoRA paragraph in Sec. 3.3 restates the
+  acceptance rule and is the form used here.
+
+Readings where the paper is silent or its indices do not close (listed with
+reasons in the design notes of the repository):
+
+* Block layout: a block of ``k`` rows is ``[anchor, r_1 .. r_{k-1}]``.  The
+  anchor is the last committed token, whose K/V is not cached yet; the
+  ``r_j`` are mask tokens (draft) or draft tokens (verify).  The speculative
+  width is k-1 (Tab. 10 uses draft length 31 with blocks of 32) and one step
+  commits between 1 and k tokens.  With k = 1 the verify pass is AR decoding.
+* Draft token d_j is the argmax of draft row j (a mask at a position predicts
+  the token at that same position, as in the diffusion objective of Sec. 2.1);
+  verify row j predicts the token at the next position (AR shift).
+* Draft mask: block rows j >= bidir_from see every block column (default 0:
+  the whole block is bidirectional); other rows are causal.
+* Decoder architecture (not specified by the paper; taken from the workload
+  statement): pre-norm RMSNorm (eps 1e-6) -> QKV -> rotate-half RoPE (base
+  1e4, angles in float64, absolute 0-based positions) -> GQA softmax attention
+  with scale 1/sqrt(head_dim) (query head h uses KV head h // (Hq/Hkv)) ->
+  O projection + residual -> RMSNorm -> SwiGLU FFN silu(h Wg) * (h Wu) ->
+  down projection + residual; final RMSNorm -> untied LM head.  No biases.
+* Argmax takes the first index of the maximum (ties to the lowest index).
+
+Arithmetic runs in float32 by default (the precision the reference oracle is
+specified in); ``dtype=np.float64`` gives a second instantiation used to
+bound this oracle's own rounding error.  Weights and cached K/V arrive as
+bfloat16 bit patterns and are widened exactly.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+DRAFT = "draft"
+VERIFY = "verify"
+
+
+# ----------------------------------------------------------------------------- elementary pieces
+def bf16_bits_to_float(bits: np.ndarray, dtype=np.float32) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns (uint16) to float32/float64."""
+    f = (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    return f.astype(dtype, copy=False)
+
+
+def rms_norm(x: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * gain over the last axis."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * gain
+
+
+def rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
+    """Rotate-half rotary embedding.
+
+    x: [..., rows, heads, D]; positions: integer array broadcastable to the
+    rows axis.  Pair (i, i + D/2) is rotated by angle pos * base^(-2i/D).
+    """
+    d = x.shape[-1]
+    half = d // 2
+    i = np.arange(half, dtype=np.float64)
+    inv_freq = base ** (-2.0 * i / d)
+    ang = np.asarray(positions, dtype=np.float64)[..., None] * inv_freq      # [..., rows, half]
+    cos = np.cos(ang).astype(x.dtype)[..., None, :]                           # [..., rows, 1, half]
+    sin = np.sin(ang).astype(x.dtype)[..., None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def softmax_attention(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, visible: np.ndarray) -> np.ndarray:
+    """softmax(q K^T / sqrt(D) restricted to visible columns) V.
+
+    q: [rows, D]; keys/vals: [n, D]; visible: bool [rows, n] (every row has at
+    least one visible column).
+    """
+    d = q.shape[-1]
+    s = (q @ keys.T) / np.sqrt(np.asarray(d, dtype=q.dtype))
+    s = np.where(visible, s, -np.inf)
+    s = s - np.max(s, axis=-1, keepdims=True)
+    p = np.exp(s)
+    p = p / np.sum(p, axis=-1, keepdims=True)
+    return p @ vals
+
+
+def block_visibility(prefix_len: int, k: int, mode: str, bidir_from: int = 0) -> np.ndarray:
+    """Which of the prefix_len + k key positions each block row may attend to.
+
+    Every block row sees the whole cached prefix (causal across blocks).  Within
+    the block, verify rows are causal (column c visible iff c <= row); draft
+    rows at or after ``bidir_from`` see every block column (bidirectional), the
+    rows before it stay causal.
+    """
+    vis = np.zeros((k, prefix_len + k), dtype=bool)
+    vis[:, :prefix_len] = True
+    for j in range(k):
+        for c in range(k):
+            if c <= j or (mode == DRAFT and j >= bidir_from):
+                vis[j, prefix_len + c] = True
+    return vis
+
+
+def argmax_first(logits: np.ndarray) -> np.ndarray:
+    """Index of the first maximum along the last axis."""
+    return np.argmax(logits, axis=-1).astype(np.int32)
+
+
+# ----------------------------------------------------------------------------- model + cache
+class OracleWeights:
+    """Float views of a synthetic model, widened from bf16 one layer at a time."""
+
+    def __init__(self, shape, source, dtype=np.float32):
+        self.shape, self.src, self.dtype = shape, source, dtype
+
+    def layer(self, l: int) -> dict:
+        w = self.src.layer(l)
+        return {name: bf16_bits_to_float(v, self.dtype) for name, v in w.items()}
+
+    def embed_rows(self, token_ids: np.ndarray) -> np.ndarray:
+        return bf16_bits_to_float(self.src.embed[np.asarray(token_ids)], self.dtype)
+
+    def final_norm(self) -> np.ndarray:
+        return bf16_bits_to_float(self.src.final_norm, self.dtype)
+
+    def lm_head(self) -> np.ndarray:
+        return bf16_bits_to_float(self.src.lm_head, self.dtype)
+
+
+class OracleKV:
+    """Per-layer K/V of every sequence plus its committed length P_b.
+
+    k[l], v[l]: [batch, n_kv_heads, capacity, head_dim] in the oracle's dtype.
+    Rows at or beyond lengths[b] are not part of the committed state.
+    """
+
+    def __init__(self, shape, batch: int, capacity: int, dtype=np.float32):
+        self.shape, self.batch, self.capacity, self.dtype = shape, batch, capacity, dtype
+        kvshape = (batch, shape.n_kv_heads, capacity, shape.head_dim)
+        self.k = [np.zeros(kvshape, dtype=dtype) for _ in range(shape.n_layers)]
+        self.v = [np.zeros(kvshape, dtype=dtype) for _ in range(shape.n_layers)]
+        self.lengths = np.zeros(batch, dtype=np.int64)
+
+    def set_prefix_bf16(self, layer: int, k_bits: np.ndarray, v_bits: np.ndarray, lengths) -> None:
+        """Load given cached K/V ([batch, kv_heads, P, D] bf16 bits) as the prefix."""
+        n = k_bits.shape[2]
+        self.k[layer][:, :, :n] = bf16_bits_to_float(k_bits, self.dtype)
+        self.v[layer][:, :, :n] = bf16_bits_to_float(v_bits, self.dtype)
+        self.lengths[:] = np.asarray(lengths)
+
+    def copy(self) -> "OracleKV":
+        c = OracleKV.__new__(OracleKV)
+        c.shape, c.batch, c.capacity, c.dtype = self.shape, self.batch, self.capacity, self.dtype
+        c.k = [a.copy() for a in self.k]
+        c.v = [a.copy() for a in self.v]
+        c.lengths = self.lengths.copy()
+        return c
+
+
+# ----------------------------------------------------------------------------- one block forward
+def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode: str,
+                  bidir_from: int = 0, positions: np.ndarray | None = None,
+                  rows_for_logits=None):
+    """One forward pass of a k-token block per sequence against the cached prefix.
+
+    tokens: int [batch, k].  Returns (logits [batch, k, vocab], new_k, new_v)
+    where new_k/new_v[l] are the block's rotated keys and values,
+    [batch, n_kv_heads, k, head_dim].  The cache itself is not modified (what
+    to commit is decided by acceptance).  ``positions`` overrides the default
+    block positions P_b + j.  ``rows_for_logits`` (optional list of row
+    indices) restricts the LM head to those rows; other rows get NaN.
+    """
+    s = weights.shape
+    dt = weights.dtype
+    tokens = np.asarray(tokens)
+    B, k = tokens.shape
+    G = s.n_q_heads // s.n_kv_heads
+    if positions is None:
+        positions = kv.lengths[:, None] + np.arange(k)[None, :]
+    positions = np.asarray(positions)
+
+    x = weights.embed_rows(tokens)                                   # [B, k, H]
+    new_k, new_v = [], []
+    for l in range(s.n_layers):
+        w = weights.layer(l)
+        h = rms_norm(x, w["attn_norm"], s.rms_eps)
+        q = (h @ w["wq"].T).reshape(B, k, s.n_q_heads, s.head_dim)
+        kb = (h @ w["wk"].T).reshape(B, k, s.n_kv_heads, s.head_dim)
+        vb = (h @ w["wv"].T).reshape(B, k, s.n_kv_heads, s.head_dim)
+        q = rope(q, positions, s.rope_base)
+        kb = rope(kb, positions, s.rope_base)
+        new_k.append(np.ascontiguousarray(kb.transpose(0, 2, 1, 3)))
+        new_v.append(np.ascontiguousarray(vb.transpose(0, 2, 1, 3)))
+
+        o = np.zeros((B, k, s.n_q_heads, s.head_dim), dtype=dt)
+        for b in range(B):
+            p_b = int(kv.lengths[b])
+            vis = block_visibility(p_b, k, mode, bidir_from)
+            for g in range(s.n_kv_heads):
+                keys = np.concatenate([kv.k[l][b, g, :p_b], kb[b, :, g]], axis=0)
+                vals = np.concatenate([kv.v[l][b, g, :p_b], vb[b, :, g]], axis=0)
+                for hq in range(g * G, (g + 1) * G):
+                    o[b, :, hq] = softmax_attention(q[b, :, hq], keys, vals, vis)
+        x = x + o.reshape(B, k, s.q_dim) @ w["wo"].T
+
+        h = rms_norm(x, w["ffn_norm"], s.rms_eps)
+        act = silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)
+        x = x + act @ w["w_down"].T
+
+    hf = rms_norm(x, weights.final_norm(), s.rms_eps)
+    lm = weights.lm_head()
+    if rows_for_logits is None:
+        logits = hf @ lm.T
+    else:
+        logits = np.full((B, k, s.vocab), np.nan, dtype=dt)
+        for r in rows_for_logits:
+            logits[:, r] = hf[:, r] @ lm.T
+    return logits, new_k, new_v
+
+
+def full_forward(weights: OracleWeights, seq_tokens: np.ndarray, visible: np.ndarray,
+                 positions: np.ndarray | None = None) -> np.ndarray:
+    """Recompute every position from tokens with an explicit attention mask (no cache).
+
+    seq_tokens: int [batch, T]; visible: bool [T, T] (row attends to column).
+    Returns logits [batch, T, vocab].  This is the plain definition the cached
+    block pass must reproduce.
+    """
+    s = weights.shape
+    B, T = seq_tokens.shape
+    G = s.n_q_heads // s.n_kv_heads
+    if positions is None:
+        positions = np.broadcast_to(np.arange(T), (B, T))
+    x = weights.embed_rows(seq_tokens)
+    for l in range(s.n_layers):
+        w = weights.layer(l)
+        h = rms_norm(x, w["attn_norm"], s.rms_eps)
+        q = rope((h @ w["wq"].T).reshape(B, T, s.n_q_heads, s.head_dim), positions, s.rope_base)
+        kk = rope((h @ w["wk"].T).reshape(B, T, s.n_kv_heads, s.head_dim), positions, s.rope_base)
+        vv = (h @ w["wv"].T).reshape(B, T, s.n_kv_heads, s.head_dim)
+        o = np.zeros((B, T, s.n_q_heads, s.head_dim), dtype=weights.dtype)
+        for b in range(B):
+            for hq in range(s.n_q_heads):
+                g = hq // G
+                o[b, :, hq] = softmax_attention(q[b, :, hq], kk[b, :, g], vv[b, :, g], visible)
+        x = x + o.reshape(B, T, s.q_dim) @ w["wo"].T
+        h = rms_norm(x, w["ffn_norm"], s.rms_eps)
+        x = x + (silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)) @ w["w_down"].T
+    return rms_norm(x, weights.final_norm(), s.rms_eps) @ weights.lm_head().T
+
+
+def sequence_visibility(prefix_len: int, k: int, mode: str, bidir_from: int = 0) -> np.ndarray:
+    """[T, T] mask for full_forward over prefix + block: causal prefix, block rows per mode."""
+    T = prefix_len + k
+    vis = np.tril(np.ones((T, T), dtype=bool))
+    vis[prefix_len:] = block_visibility(prefix_len, k, mode, bidir_from)
+    return vis
+
+
+# ----------------------------------------------------------------------------- decoding steps
+def accept(draft: np.ndarray, ar_pred: np.ndarray):
+    """Longest-prefix acceptance with one bonus token, for one sequence.
+
+    draft[j-1] = d_j (j = 1..k-1) are the draft tokens at positions P+1..P+k-1;
+    ar_pred[j] = a_j is the AR prediction of verify row j, i.e. for position
+    P+j+1.  With j* the first j where d_j != a_{j-1}, the accepted length is
+    L = j* - 1, or k - 1 when no mismatch exists.  The committed tokens are
+    d_1..d_L followed by the bonus a_L (the AR token at the first rejected
+    position, or after the last draft).  Returns (L, committed list, bonus).
+    """
+    k = len(ar_pred)
+    j_star = None
+    for j in range(1, k):
+        if draft[j - 1] != ar_pred[j - 1]:
+            j_star = j
+            break
+    L = (k - 1) if j_star is None else j_star - 1
+    bonus = int(ar_pred[L])
+    committed = [int(t) for t in draft[:L]] + [bonus]
+    return L, committed, bonus
+
+
+def commit(kv: OracleKV, new_k, new_v, n_rows) -> None:
+    """Append the first n_rows[b] block rows of every layer to the cache."""
+    for b in range(kv.batch):
+        p, n = int(kv.lengths[b]), int(n_rows[b])
+        if p + n > kv.capacity:
+            raise ValueError("cache capacity exceeded")
+        for l in range(len(new_k)):
+            kv.k[l][b, :, p:p + n] = new_k[l][b, :, :n]
+            kv.v[l][b, :, p:p + n] = new_v[l][b, :, :n]
+        kv.lengths[b] = p + n
+
+
+def draft_block(anchor: np.ndarray, k: int, mask_id: int) -> np.ndarray:
+    """[anchor, mask x (k-1)] per sequence."""
+    blk = np.full((len(anchor), k), mask_id, dtype=np.int32)
+    blk[:, 0] = anchor
+    return blk
+
+
+def verify_block(anchor: np.ndarray, drafts: np.ndarray) -> np.ndarray:
+    """[anchor, d_1 .. d_{k-1}] per sequence."""
+    return np.concatenate([np.asarray(anchor, dtype=np.int32)[:, None],
+                           np.asarray(drafts, dtype=np.int32)], axis=1)
+
+
+def draft_pass(weights, kv, anchor, k, bidir_from=0):
+    """Diffusion draft: d_j = argmax of draft row j for j = 1..k-1.  Returns (drafts, logits)."""
+    logits, _, _ = block_forward(weights, kv, draft_block(anchor, k, weights.shape.mask_token_id),
+                                 DRAFT, bidir_from)
+    return argmax_first(logits)[:, 1:], logits
+
+
+def verify_pass(weights, kv, anchor, drafts):
+    """AR verify over [anchor, drafts] with the causal mask.  Returns (a, logits, new_k, new_v)."""
+    logits, nk, nv = block_forward(weights, kv, verify_block(anchor, drafts), VERIFY)
+    return argmax_first(logits), logits, nk, nv
+
+
+def self_spec_step(weights, kv, anchor, k, bidir_from=0):
+    """One linear self-speculation step; commits accepted rows into ``kv``.
+
+    Returns dict with drafts, verify argmax, accept lengths L, committed tokens
+    (per sequence lists) and the next anchors.
+    """
+    drafts, dlogits = draft_pass(weights, kv, anchor, k, bidir_from)
+    a, vlogits, nk, nv = verify_pass(weights, kv, anchor, drafts)
+    Ls, committed, nxt = [], [], []
+    for b in range(len(anchor)):
+        L, c, bonus = accept(drafts[b], a[b])
+        Ls.append(L)
+        committed.append(c)
+        nxt.append(bonus)
+    commit(kv, nk, nv, np.asarray(Ls) + 1)
+    return {"drafts": drafts, "ar": a, "L": np.asarray(Ls, dtype=np.int32), "committed": committed,
+            "next_anchor": np.asarray(nxt, dtype=np.int32), "draft_logits": dlogits, "verify_logits": vlogits}
+
+
+def ar_step(weights, kv, token):
+    """Mode 1: one AR decoding step (a one-token verify pass) that commits its row."""
+    logits, nk, nv = block_forward(weights, kv, np.asarray(token, dtype=np.int32)[:, None], VERIFY)
+    commit(kv, nk, nv, np.ones(kv.batch, dtype=np.int64))
+    return argmax_first(logits)[:, 0], logits
+
+
+def prefill(weights, kv, prefix_tokens, chunk: int = 0):
+    """Causal prefill of a token prefix into an empty cache (verify passes, all rows committed)."""
+    prefix_tokens = np.asarray(prefix_tokens, dtype=np.int32)
+    T = prefix_tokens.shape[1]
+    chunk = chunk or T
+    for c0 in range(0, T, chunk):
+        blk = prefix_tokens[:, c0:c0 + chunk]
+        _, nk, nv = block_forward(weights, kv, blk, VERIFY)
+        commit(kv, nk, nv, np.full(kv.batch, blk.shape[1]))

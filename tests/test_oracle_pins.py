@@ -1,0 +1,354 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix (no GPU).
+
+Each test names the invariant it pins.  A plausible mistake in the oracle
+(wrong mask, wrong RoPE pairing or position, transposed weight, wrong GQA
+grouping, off-by-one in acceptance) fails at least one of them.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import nld_oracle as O
+from synth.workloads import LazyWeights, ModelShape, SHAPE_TINY, tokens as synth_tokens
+
+# a small decoder for fast pins: 2 layers, GQA group 2, odd vocab
+MINI = ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96, vocab=97)
+
+
+def mini_weights(dtype=np.float64, seed=11, shape=MINI):
+    return O.OracleWeights(shape, LazyWeights(shape, seed), dtype)
+
+
+def prefilled(w, prefix_tokens, capacity=None):
+    kv = O.OracleKV(w.shape, prefix_tokens.shape[0], capacity or prefix_tokens.shape[1] + 40, w.dtype)
+    O.prefill(w, kv, prefix_tokens)
+    return kv
+
+
+def rel(a, b):
+    return float(np.max(np.abs(a - b)) / np.max(np.abs(b)))
+
+
+# ----------------------------------------------------------------------------- elementary closed forms
+def test_rope_hand_example(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "rope_d4_pos1.json")))
+    x = np.array(g["x"], dtype=np.float64).reshape(1, 1, 4)
+    out = O.rope(x, np.array([g["position"]]), g["base"]).reshape(-1)
+    np.testing.assert_allclose(out, g["expected"], rtol=0, atol=1e-15)
+
+
+def test_rope_identity_norm_and_relative_position():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((3, 2, 16))
+    np.testing.assert_array_equal(O.rope(x, np.zeros(3, dtype=int), 1e4), x)        # position 0 = identity
+    r = O.rope(x, np.array([5, 900, 70000]), 1e4)
+    np.testing.assert_allclose(np.linalg.norm(r, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    # <rope(q, m), rope(k, n)> depends only on m - n
+    q, k = rng.standard_normal((1, 1, 16)), rng.standard_normal((1, 1, 16))
+    d1 = np.sum(O.rope(q, np.array([17]), 1e4) * O.rope(k, np.array([5]), 1e4))
+    d2 = np.sum(O.rope(q, np.array([1012]), 1e4) * O.rope(k, np.array([1000]), 1e4))
+    assert abs(d1 - d2) < 1e-11
+
+
+def test_rmsnorm_and_swiglu_closed_forms():
+    c = np.full((1, 8), 3.0)
+    np.testing.assert_allclose(O.rms_norm(c, np.full(8, 2.0), 1e-6), 2 * 3 / np.sqrt(9 + 1e-6), rtol=1e-15)
+    np.testing.assert_allclose(O.rms_norm(np.array([[3.0, 4.0]]), np.ones(2), 0.0),
+                               [[3 / np.sqrt(12.5), 4 / np.sqrt(12.5)]], rtol=1e-15)
+    assert O.silu(np.array(0.0)) == 0.0
+    np.testing.assert_allclose(O.silu(np.array([40.0, -40.0, 1.0])), [40.0, 0.0, 1 / (1 + np.exp(-1))], atol=1e-15)
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(1)
+    v = rng.standard_normal((6, 4))
+    keys = np.tile(rng.standard_normal((1, 4)), (6, 1))            # all keys equal -> uniform weights
+    q = rng.standard_normal((3, 4))
+    vis = O.block_visibility(3, 3, O.VERIFY)                         # rows see 4, 5, 6 keys
+    out = O.softmax_attention(q, keys, v, vis)
+    for j in range(3):
+        np.testing.assert_allclose(out[j], v[:4 + j].mean(axis=0), rtol=1e-13)
+    vis1 = np.zeros((3, 6), dtype=bool)
+    vis1[:, 2] = True                                                # one visible key -> its value
+    np.testing.assert_allclose(O.softmax_attention(q, rng.standard_normal((6, 4)), v, vis1), np.tile(v[2], (3, 1)))
+
+
+def test_block_visibility_patterns():
+    v = O.block_visibility(2, 3, O.VERIFY)
+    assert v.tolist() == [[1, 1, 1, 0, 0], [1, 1, 1, 1, 0], [1, 1, 1, 1, 1]]
+    assert O.block_visibility(2, 3, O.DRAFT).all()
+    d1 = O.block_visibility(2, 3, O.DRAFT, bidir_from=1)
+    assert d1.tolist() == [[1, 1, 1, 0, 0], [1, 1, 1, 1, 1], [1, 1, 1, 1, 1]]
+
+
+def test_argmax_ties_and_signed_zero():
+    assert O.argmax_first(np.array([1.0, 3.0, 3.0, 2.0])) == 1
+    assert O.argmax_first(np.array([-0.0, 0.0])) == 0
+    assert O.argmax_first(np.array([0.0, -0.0])) == 0
+    assert O.argmax_first(np.array([-1.0, -0.0, 0.0, -2.0])) == 1
+    assert O.argmax_first(np.full(7, 0.25)) == 0
+
+
+# ----------------------------------------------------------------------------- acceptance rule
+def test_accept_hand_examples(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "accept_examples.json")))
+    for c in g["cases"]:
+        L, committed, bonus = O.accept(np.array(c["draft"], dtype=int), np.array(c["ar"], dtype=int))
+        assert L == c["L"] and committed == c["committed"] and bonus == c["committed"][-1], c
+
+
+@pytest.mark.parametrize("V,k", [(2, 1), (2, 2), (2, 4), (3, 3), (3, 4), (4, 3)])
+def test_accept_exhaustive_brute_force(V, k):
+    """Every (draft, AR) pair over a tiny vocabulary: L is the longest matching prefix."""
+    for draft in itertools.product(range(V), repeat=k - 1):
+        for ar in itertools.product(range(V), repeat=k):
+            L, committed, bonus = O.accept(np.array(draft, dtype=int), np.array(ar, dtype=int))
+            longest = max(l for l in range(k) if list(draft[:l]) == list(ar[:l]))
+            assert L == longest
+            assert committed == list(draft[:L]) + [ar[L]] and bonus == ar[L]
+            assert 1 <= len(committed) <= k
+
+
+# ----------------------------------------------------------------------------- the block pass
+@pytest.fixture(scope="module")
+def mini():
+    w = mini_weights()
+    prefix = synth_tokens(MINI, 5, "pin.prefix", (2, 13))
+    block = synth_tokens(MINI, 5, "pin.block", (2, 6))
+    return w, prefix, block
+
+
+def test_verify_k1_equals_ar_full_recompute(mini):
+    """P1: a one-token verify pass over the cache equals plain causal decoding recomputed from tokens."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    logits, _, _ = O.block_forward(w, kv, block[:, :1], O.VERIFY)
+    seq = np.concatenate([prefix, block[:, :1]], axis=1)
+    full = O.full_forward(w, seq, np.tril(np.ones((14, 14), dtype=bool)))
+    np.testing.assert_allclose(logits[:, 0], full[:, -1], rtol=1e-10, atol=1e-12)
+
+
+def test_verify_equals_sequential_ar_steps(mini):
+    """P2: one causal verify pass over k tokens equals k teacher-forced one-token steps (logits and K/V)."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    logits, nk, nv = O.block_forward(w, kv, block, O.VERIFY)
+    kv2 = kv.copy()
+    for j in range(block.shape[1]):
+        _, lj = O.ar_step(w, kv2, block[:, j])
+        np.testing.assert_allclose(logits[:, j], lj[:, 0], rtol=1e-10, atol=1e-12)
+    P = prefix.shape[1]
+    for l in range(MINI.n_layers):
+        np.testing.assert_allclose(kv2.k[l][:, :, P:P + 6], nk[l], rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(kv2.v[l][:, :, P:P + 6], nv[l], rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("bidir_from", [0, 1, 3])
+def test_draft_equals_full_attention(mini, bidir_from):
+    """P3: the draft pass equals full recompute over [prefix ; block] with the block rows bidirectional."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    logits, _, _ = O.block_forward(w, kv, block, O.DRAFT, bidir_from)
+    seq = np.concatenate([prefix, block], axis=1)
+    full = O.full_forward(w, seq, O.sequence_visibility(13, 6, O.DRAFT, bidir_from))
+    np.testing.assert_allclose(logits, full[:, 13:], rtol=1e-10, atol=1e-12)
+    causal = O.full_forward(w, seq, O.sequence_visibility(13, 6, O.VERIFY))
+    assert rel(full[:, 13:], causal[:, 13:]) > 1e-3          # the masks really differ
+
+
+def test_draft_mask_degenerate_cases(mini):
+    """P4: draft with k=1, or with bidir_from=k, is exactly the verify pass."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    a = O.block_forward(w, kv, block[:, :1], O.DRAFT)[0]
+    b = O.block_forward(w, kv, block[:, :1], O.VERIFY)[0]
+    np.testing.assert_array_equal(a, b)
+    a = O.block_forward(w, kv, block, O.DRAFT, bidir_from=6)[0]
+    b = O.block_forward(w, kv, block, O.VERIFY)[0]
+    np.testing.assert_array_equal(a, b)
+
+
+def test_verify_rows_ignore_later_rows(mini):
+    """P5: verify row i does not depend on block tokens at rows > i (causality)."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    base = O.block_forward(w, kv, block, O.VERIFY)[0]
+    changed = block.copy()
+    changed[:, 4:] = (changed[:, 4:] + 7) % (MINI.vocab - 1)
+    alt = O.block_forward(w, kv, changed, O.VERIFY)[0]
+    np.testing.assert_allclose(alt[:, :4], base[:, :4], rtol=1e-12, atol=1e-13)
+    assert rel(alt[:, 4:], base[:, 4:]) > 1e-3
+    alt_d = O.block_forward(w, kv, changed, O.DRAFT)[0]
+    base_d = O.block_forward(w, kv, block, O.DRAFT)[0]
+    assert rel(alt_d[:, :4], base_d[:, :4]) > 1e-4            # the draft rows do see later rows
+
+
+def test_draft_permutation_equivariance(mini):
+    """P6: permuting block tokens together with their positions permutes the draft rows."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    P = prefix.shape[1]
+    pos = P + np.arange(6)[None, :].repeat(2, axis=0)
+    perm = np.array([3, 0, 5, 1, 4, 2])
+    base = O.block_forward(w, kv, block, O.DRAFT, positions=pos)[0]
+    alt = O.block_forward(w, kv, block[:, perm], O.DRAFT, positions=pos[:, perm])[0]
+    np.testing.assert_allclose(alt, base[:, perm], rtol=1e-10, atol=1e-12)
+
+
+def test_position_shift_invariance():
+    """P7: shifting every position of prefix and block by a constant leaves the logits unchanged."""
+    w = mini_weights()
+    seq = synth_tokens(MINI, 6, "pin.shift", (1, 10))
+    vis = O.sequence_visibility(7, 3, O.DRAFT)
+    a = O.full_forward(w, seq, vis, positions=np.arange(10)[None])
+    b = O.full_forward(w, seq, vis, positions=1000 + np.arange(10)[None])
+    np.testing.assert_allclose(a, b, rtol=1e-8, atol=1e-10)
+
+
+def test_gqa_equals_mha_with_replicated_kv_heads(mini):
+    """GQA grouping: query head h reads KV head h // (Hq/Hkv); equal to MHA with replicated K/V projections."""
+    w, prefix, block = mini
+    mha_shape = ModelShape(**{**MINI.__dict__, "n_kv_heads": MINI.n_q_heads})
+
+    class Replicated:
+        def __init__(self, src):
+            self.src = src
+            self.embed, self.lm_head, self.final_norm = src.embed, src.lm_head, src.final_norm
+
+        def layer(self, l):
+            d = dict(self.src.layer(l))
+            G, D = MINI.n_q_heads // MINI.n_kv_heads, MINI.head_dim
+            for name in ("wk", "wv"):
+                heads = d[name].reshape(MINI.n_kv_heads, D, MINI.hidden)
+                d[name] = np.repeat(heads, G, axis=0).reshape(-1, MINI.hidden)
+            return d
+
+    wm = O.OracleWeights(mha_shape, Replicated(LazyWeights(MINI, 11)), np.float64)
+    seq = np.concatenate([prefix, block], axis=1)
+    vis = O.sequence_visibility(13, 6, O.VERIFY)
+    np.testing.assert_allclose(O.full_forward(w, seq, vis), O.full_forward(wm, seq, vis), rtol=1e-10, atol=1e-12)
+
+
+def _torch_reference_logits(shape, src, seq, visible):
+    """The same decoder written with PyTorch library routines (F.linear's [out][in] weights, F.rms_norm,
+    scaled_dot_product_attention with an explicit mask, F.silu) and RoPE as a complex rotation."""
+    def t(bits):
+        return torch.from_numpy(O.bf16_bits_to_float(bits, np.float64))
+
+    T = seq.shape[1]
+    D, half = shape.head_dim, shape.head_dim // 2
+    inv = torch.tensor([shape.rope_base ** (-2.0 * i / D) for i in range(half)], dtype=torch.float64)
+    rot = torch.polar(torch.ones(T, half, dtype=torch.float64), torch.arange(T, dtype=torch.float64)[:, None] * inv)
+
+    def rope_c(x):                                   # x [B, T, H, D]; pair (i, i+D/2) as one complex number
+        z = torch.complex(x[..., :half], x[..., half:]) * rot[None, :, None, :]
+        return torch.cat([z.real, z.imag], dim=-1)
+
+    x = t(src.embed)[torch.from_numpy(seq.astype(np.int64))]
+    mask = torch.from_numpy(visible)
+    G = shape.n_q_heads // shape.n_kv_heads
+    for l in range(shape.n_layers):
+        w = {k: t(v) for k, v in src.layer(l).items()}
+        h = F.rms_norm(x, (shape.hidden,), w["attn_norm"], eps=shape.rms_eps)
+        B = x.shape[0]
+        q = rope_c(F.linear(h, w["wq"]).view(B, T, shape.n_q_heads, D)).transpose(1, 2)
+        k = rope_c(F.linear(h, w["wk"]).view(B, T, shape.n_kv_heads, D)).transpose(1, 2)
+        v = F.linear(h, w["wv"]).view(B, T, shape.n_kv_heads, D).transpose(1, 2)
+        k = k.repeat_interleave(G, dim=1)
+        v = v.repeat_interleave(G, dim=1)
+        o = F.scaled_dot_product_attention(q, k, v, attn_mask=mask).transpose(1, 2).reshape(B, T, -1)
+        x = x + F.linear(o, w["wo"])
+        h = F.rms_norm(x, (shape.hidden,), w["ffn_norm"], eps=shape.rms_eps)
+        x = x + F.linear(F.silu(F.linear(h, w["w_gate"])) * F.linear(h, w["w_up"]), w["w_down"])
+    x = F.rms_norm(x, (shape.hidden,), t(src.final_norm), eps=shape.rms_eps)
+    return F.linear(x, t(src.lm_head)).numpy()
+
+
+@pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
+def test_block_pass_matches_torch_library_decoder(mini, mode):
+    """The cached block pass equals the decoder built from PyTorch library layers (weight layout,
+    norm placement, SwiGLU, GQA and attention masking)."""
+    w, prefix, block = mini
+    kv = prefilled(w, prefix)
+    logits = O.block_forward(w, kv, block, mode)[0]
+    seq = np.concatenate([prefix, block], axis=1)
+    ref = _torch_reference_logits(MINI, LazyWeights(MINI, 11), seq, O.sequence_visibility(13, 6, mode))
+    np.testing.assert_allclose(logits, ref[:, 13:], rtol=1e-9, atol=1e-11)
+
+
+def test_fp32_oracle_close_to_fp64():
+    """P13: on the tiny workload the float32 oracle is within 1e-4 (normwise) of the float64 one."""
+    src = LazyWeights(SHAPE_TINY, 0)
+    prefix = synth_tokens(SHAPE_TINY, 0, "pin.p13.prefix", (1, 32))
+    block = synth_tokens(SHAPE_TINY, 0, "pin.p13.block", (1, 8))
+    outs = []
+    for dt in (np.float32, np.float64):
+        w = O.OracleWeights(SHAPE_TINY, src, dt)
+        kv = prefilled(w, prefix)
+        outs.append(O.block_forward(w, kv, block, O.DRAFT)[0])
+    assert rel(outs[0].astype(np.float64), outs[1]) < 1e-4
+
+
+# ----------------------------------------------------------------------------- decoding loop
+def test_self_speculation_reproduces_greedy_ar():
+    """Greedy verification makes self-speculation commit exactly the greedy AR continuation, and the
+    cache it builds equals the one AR decoding builds (only accepted rows are committed)."""
+    w = mini_weights()
+    prefix = synth_tokens(MINI, 9, "pin.ss.prefix", (2, 9))
+    k, steps = 5, 4
+    kv_ss = prefilled(w, prefix[:, :-1], capacity=64)
+    kv_ar = kv_ss.copy()
+    anchor = prefix[:, -1].copy()
+    out_ss = [[] for _ in range(2)]
+    for _ in range(steps):
+        r = O.self_spec_step(w, kv_ss, anchor, k)
+        for b in range(2):
+            assert 0 <= r["L"][b] <= k - 1
+            out_ss[b] += r["committed"][b]
+        anchor = r["next_anchor"]
+    n = min(len(o) for o in out_ss)
+    tok = prefix[:, -1].copy()
+    out_ar = [[] for _ in range(2)]
+    for _ in range(n):
+        tok, _ = O.ar_step(w, kv_ar, tok)
+        for b in range(2):
+            out_ar[b].append(int(tok[b]))
+    for b in range(2):
+        assert out_ss[b][:n] == out_ar[b]
+
+
+def test_planted_drafts_are_fully_accepted():
+    """Drafts equal to the greedy AR continuation are accepted in full (L = k-1), the bonus is the next
+    AR token, and the committed cache rows equal those of AR decoding."""
+    w = mini_weights()
+    prefix = synth_tokens(MINI, 10, "pin.plant.prefix", (1, 9))
+    k = 6
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    kv_ar = kv.copy()
+    tok, greedy = prefix[:, -1].copy(), []
+    for _ in range(k):
+        tok, _ = O.ar_step(w, kv_ar, tok)
+        greedy.append(int(tok[0]))
+    a, _, nk, nv = O.verify_pass(w, kv, prefix[:, -1], np.array([greedy[:k - 1]]))
+    L, committed, bonus = O.accept(np.array(greedy[:k - 1]), a[0])
+    assert L == k - 1 and committed == greedy and bonus == greedy[-1]
+    O.commit(kv, nk, nv, [L + 1])
+    for l in range(MINI.n_layers):
+        np.testing.assert_allclose(kv.k[l][:, :, :int(kv.lengths[0])], kv_ar.k[l][:, :, :int(kv.lengths[0])],
+                                   rtol=1e-10, atol=1e-12)
+
+
+def test_chunked_prefill_equals_single_pass():
+    w = mini_weights()
+    prefix = synth_tokens(MINI, 12, "pin.chunk", (1, 20))
+    a = prefilled(w, prefix)
+    b = O.OracleKV(MINI, 1, 60, np.float64)
+    O.prefill(w, b, prefix, chunk=7)
+    for l in range(MINI.n_layers):
+        np.testing.assert_allclose(a.k[l], b.k[l], rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(a.v[l], b.v[l], rtol=1e-10, atol=1e-12)
