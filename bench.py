@@ -1,0 +1,245 @@
+"""Benchmark of the block-decode step (draft pass + verify pass + acceptance) on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload 8b] [--no-cpu-baseline]
+
+A step is one linear self-speculation step over the synthetic workload: the
+diffusion draft pass over [anchor, mask x (k-1)], the causal verify pass over
+[anchor, drafts], the argmax, the longest-prefix acceptance and the commit of
+the accepted rows, all on the device (the next step's anchor stays on the
+device).  The timed steps replay one captured HIP graph.
+
+value = block tokens pushed through block-decode passes per second
+      = 2 passes x batch x k per step / step time.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "block-decode tokens/sec at 1 MI355X; % of HBM roofline (8B-shape, k=16, bs=1)"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def kernel_bytes(shape, batch, k, prefix_lens):
+    """Algorithmic HBM bytes per launch of each kernel class: bf16 weights once, K/V read once,
+    activations read and written once."""
+    M, H, F, V = batch * k, shape.hidden, shape.ffn, shape.vocab
+    QD, KVD = shape.q_dim, shape.kv_dim
+    kv_keys = int(np.sum(np.asarray(prefix_lens) + k))
+    return {
+        "embed": M * H * (2 + 4 + 2),
+        "qkv": 2 * H * (QD + 2 * KVD) + 2 * M * H + 2 * M * QD + 2 * 2 * M * KVD,
+        "attention": 2 * 2 * kv_keys * KVD + 2 * M * QD * 2,
+        "o_proj": 2 * QD * H + 2 * M * QD + 4 * M * H * 2 + 2 * M * H,
+        "gate_up": 2 * H * 2 * F + 2 * M * H + 2 * M * F,
+        "down": 2 * F * H + 2 * M * F + 4 * M * H * 2 + 2 * M * H,
+        "lm_head": 2 * V * H + 2 * M * H,
+        "argmax": 0,
+    }
+
+
+def pass_bytes(shape, batch, k, prefix_lens):
+    kb = kernel_bytes(shape, batch, k, prefix_lens)
+    return kb["embed"] + shape.n_layers * (kb["qkv"] + kb["attention"] + kb["o_proj"] + kb["gate_up"] + kb["down"]) \
+        + kb["lm_head"]
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [d.get("num_threads", 0) for d in threadpool_info() if d.get("user_api") == "blas"]
+        return max(n) if n else os.cpu_count()
+    except Exception:
+        return os.cpu_count()
+
+
+def cpu_baseline(wl, k, sample_layers=(2, 4)):
+    """Time the CPU oracle's verify pass on the first few layers + LM head; extrapolate linearly in layers."""
+    from oracle import nld_oracle as O
+    from synth.workloads import LazyWeights, ModelShape, prefix_kv, tokens
+
+    shape = wl.shape
+    P = int(wl.prefix_lengths()[0])
+    times = {}
+    for nl in sample_layers:
+        sub = ModelShape(**{**shape.__dict__, "n_layers": nl})
+        src = LazyWeights(sub, wl.seed, keep=True)
+        for l in range(nl):
+            src.layer(l)
+        _ = src.embed, src.lm_head
+        w = O.OracleWeights(sub, src, np.float32)
+        kv = O.OracleKV(sub, 1, P + k, np.float32)
+        for l in range(nl):
+            kb, vb = prefix_kv(shape, wl.seed, l, 1, P)
+            kv.set_prefix_bf16(l, kb, vb, [P])
+        blk = tokens(shape, wl.seed, "bench.cpu.block", (1, k))
+        t0 = time.perf_counter()
+        O.block_forward(w, kv, blk, O.VERIFY)
+        times[nl] = time.perf_counter() - t0
+        log("oracle pass with %d layers + LM head: %.2f s" % (nl, times[nl]))
+    a, b = sample_layers
+    per_layer = max((times[b] - times[a]) / (b - a), 1e-9)
+    t_pass = times[b] + (shape.n_layers - b) * per_layer
+    return {
+        "value": round(k / t_pass, 4), "unit": "block tokens/s", "cores": int(blas_threads()), "kind": "oracle",
+        "sample": "fp32 numpy oracle, one verify pass (batch 1, k=%d, prefix %d) over the first %d and %d of %d "
+                  "layers + LM head (%.1f s, %.1f s); full pass extrapolated linearly in layers: %.1f s"
+                  % (k, P, a, b, shape.n_layers, times[a], times[b], t_pass),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="8b")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_05722_amd import _lib as C
+    from paper_2607_05722_amd import runtime as R
+    from synth.workloads import LazyWeights, WORKLOADS, prefix_kv, tokens
+
+    wl = WORKLOADS[args.workload]
+    shape, k, B = wl.shape, wl.k_values[0], wl.batch
+    plens = wl.prefix_lengths()
+    steps, warmup = args.steps, args.warmup
+    max_len = int(-(-(int(plens.max()) + (steps + warmup + 4) * k) // 64) * 64)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.perf_counter()
+    model = R.DeviceModel(shape, LazyWeights(shape, wl.seed, keep=False))
+    log("weights generated, uploaded and packed in %.1f s" % (time.perf_counter() - t0))
+    cache = R.DeviceCache(shape, B, max_len)
+    for l in range(shape.n_layers):
+        kb, vb = prefix_kv(shape, wl.seed, l, B, int(plens.max()))
+        cache.load_prefix(l, kb, vb)
+    cache.set_lengths(plens)
+    ws = R.Workspace(model, B, k, max_len)
+    anchor = torch.from_numpy(tokens(shape, wl.seed, "bench.anchor", (B,))).to(dev)
+    drafts = torch.empty((B, k - 1), dtype=torch.int32, device=dev)
+    outs = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+            "committed": torch.empty((B, k), dtype=torch.int32, device=dev),
+            "next_anchor": anchor}                        # in place: the loop never leaves the device
+    torch.cuda.synchronize()
+    log("cache filled (prefix %s), max_len %d, workspace %.1f MB" % (
+        plens.tolist() if B <= 4 else "%d..%d" % (plens.min(), plens.max()), max_len, ws.nbytes / 1e6))
+
+    committed_total = torch.zeros(1, dtype=torch.int64, device=dev)
+
+    def step():
+        R.draft(model, cache, ws, anchor, k, out=drafts)
+        R.verify_accept(model, cache, ws, anchor, drafts, k, outs=outs)
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        graph = None
+        if not args.no_graph:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                step()
+            graph.replay()
+        torch.cuda.synchronize()
+        len0 = cache.lengths.clone()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            if graph is not None:
+                graph.replay()
+            else:
+                step()
+        e1.record()
+        torch.cuda.synchronize()
+        elapsed_ms = e0.elapsed_time(e1)
+        committed = int((cache.lengths - len0).sum().item())
+        status = R.read_device_status(ws)
+
+        # per-kernel durations, HIP events on this stream around every launch of a few eager steps
+        lib = C.load()
+        lib.nld_trace_enable(1)
+        trace_steps = 3
+        for _ in range(trace_steps):
+            step()
+        torch.cuda.synchronize()
+        import ctypes
+        ms = (ctypes.c_float * 8)()
+        cnt = (ctypes.c_int32 * 8)()
+        C.check(lib.nld_trace_read(ms, cnt, 8))
+        lib.nld_trace_enable(0)
+
+    ms_per_step = elapsed_ms / steps
+    value = 2.0 * B * k / (ms_per_step * 1e-3)
+    bytes_step = 2 * pass_bytes(shape, B, k, plens)
+    kb = kernel_bytes(shape, B, k, plens)
+    kernels = {}
+    for i, name in enumerate(C.TRACE_CLASSES):
+        if cnt[i]:
+            avg_ms = ms[i] / cnt[i]
+            kernels[name] = {"avg_us": round(avg_ms * 1e3, 2), "launches_per_step": cnt[i] // trace_steps,
+                             "GBps": round(kb[name] / (avg_ms * 1e-3) / 1e9, 1) if kb[name] else None}
+    dom = max((n for n in kernels), key=lambda n: kernels[n]["avg_us"] * kernels[n]["launches_per_step"])
+    dom_avg_s = kernels[dom]["avg_us"] * 1e-6
+    achieved = kb[dom] / dom_avg_s / 1e9
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "block tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "%s: %d layers, hidden %d, %d/%d heads, head_dim %d, ffn %d, vocab %d; batch %d, "
+                               "prefix %s, block k=%d; step = draft pass + verify pass + accept"
+                               % (wl.name, shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads,
+                                  shape.head_dim, shape.ffn, shape.vocab, B,
+                                  int(plens[0]) if wl.ragged is None else "ragged %d..%d" % wl.ragged, k),
+                   "graph": graph is not None},
+        "pass_ms": round(ms_per_step / 2, 4),
+        "step_hbm_GBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "algorithmic_bytes_per_step": int(bytes_step),
+        "committed_tokens_per_s": round(committed / (elapsed_ms * 1e-3), 1),
+        "device_status": status,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": int(kb[dom]), "avg_launch_us": kernels[dom]["avg_us"]},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        del model, cache, ws
+        torch.cuda.empty_cache()
+        res["cpu_baseline"] = cpu_baseline(wl, k)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

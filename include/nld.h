@@ -1,0 +1,241 @@
+/*
+ * nld.h -- block-decode step of linear self-speculation on AMD MI355X (gfx950).
+ *
+ * Method: arXiv 2607.05722, Sec. 3.3 ("Mode 3: Self-Speculation Decoding",
+ * linear self-speculation).  A block of k tokens per sequence runs one
+ * forward pass of a decoder-only transformer against the sequence's prefix
+ * KV cache.  In the diffusion *draft* pass the block attends bidirectionally
+ * within itself (block-wise diffusion, Sec. 2.1); in the AR *verify* pass it
+ * is causal (Sec. 2.2, Sec. 3.1).  The longest draft prefix that matches the
+ * AR predictions is accepted and the AR prediction at the first rejected
+ * position is committed as one extra token (Sec. 3.3; the first-mismatch
+ * index j* of the same section).
+ *
+ * Block layout.  Row 0 of a block is the *anchor*: the last committed token,
+ * whose K/V is not cached yet.  Rows 1..k-1 hold mask tokens (draft) or the
+ * draft tokens d_1..d_{k-1} (verify), so the speculative width is k-1 (the
+ * paper's Tab. 10 pairs draft length 31 with blocks of 32).  Block row j sits
+ * at absolute position P_b + j, where P_b is the sequence's committed length.
+ * Draft token d_j is the argmax of draft row j; verify row j predicts the
+ * token at position P_b + j + 1.  A step commits L+1 tokens, 0 <= L <= k-1.
+ *
+ * Conventions for every call:
+ *  - All array arguments are DEVICE pointers unless marked "host".  The
+ *    caller allocates and owns every buffer (weights, cache, workspace,
+ *    outputs); the library never allocates or frees device memory and keeps
+ *    no pointer after a call returns, except the weight pointers a model
+ *    handle borrows (they must outlive the handle).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Calls only enqueue work; they never synchronize except
+ *    nld_read_device_status.
+ *  - bf16 means IEEE bfloat16 bit patterns (uint16).  Matrices are row-major.
+ *  - Argument checks run on the host before anything is enqueued; a failing
+ *    call enqueues nothing and returns a negative nld_status, with a message
+ *    available from nld_last_error() (thread-local).
+ *  - Conditions only the device can see (a token id outside [0, vocab), a
+ *    block that would run past the cache capacity, max_len < P_b + k) set bits
+ *    of a sticky status word in the workspace; the offending write is
+ *    skipped, never performed out of bounds.  Read it with
+ *    nld_read_device_status.
+ *  - Concurrent calls on one workspace race; give each stream its own.
+ */
+#ifndef NLD_H
+#define NLD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NLD_OK = 0,
+    NLD_ERR_INVALID_ARG = -1,   /* null pointer, non-positive size, value out of range */
+    NLD_ERR_SHAPE = -2,         /* a size the kernels do not support (see each call) */
+    NLD_ERR_CAPACITY = -3,      /* workspace too small */
+    NLD_ERR_HIP = -4,           /* a HIP runtime call failed; message has the HIP error */
+    NLD_ERR_UNSUPPORTED = -5,   /* no gfx950 device, or an unsupported mode */
+    NLD_ERR_DEVICE = -6         /* nld_read_device_status found a device-side error bit */
+} nld_status;
+
+/* Device status bits (sticky, OR-ed together). */
+#define NLD_DEV_BAD_TOKEN 0x1u     /* a token id outside [0, vocab) was replaced by 0 */
+#define NLD_DEV_CAPACITY 0x2u      /* P_b + k > max_len: the block's K/V rows were not written */
+#define NLD_DEV_BAD_LENGTH 0x4u    /* a negative committed length was read */
+
+typedef enum {
+    NLD_MODE_VERIFY = 0,   /* AR verify: causal within the block */
+    NLD_MODE_DRAFT = 1     /* diffusion draft: block rows >= bidir_from see the whole block */
+} nld_mode;
+
+/* Architecture of the decoder.  Pre-norm RMSNorm, rotate-half RoPE (pairs
+ * (i, i + head_dim/2), angle pos * rope_base^(-2i/head_dim)), GQA attention
+ * with scale 1/sqrt(head_dim) where query head h reads KV head
+ * h / (n_q_heads / n_kv_heads), SwiGLU FFN silu(x Wg) * (x Wu) then Wd,
+ * residual connections, final RMSNorm, untied LM head; no biases. */
+typedef struct {
+    int32_t n_layers;
+    int32_t hidden;        /* multiple of 32 */
+    int32_t n_q_heads;
+    int32_t n_kv_heads;    /* divides n_q_heads */
+    int32_t head_dim;      /* 64 or 128 */
+    int32_t ffn;           /* multiple of 8 */
+    int32_t vocab;
+    float rope_base;
+    float rms_eps;
+    int32_t mask_token_id; /* token placed in draft rows 1..k-1 */
+} nld_config;
+
+/* Per-layer weights.  Norm gains are plain bf16 vectors; matrices must be in
+ * the packed layouts produced by the nld_pack_* calls below. */
+typedef struct {
+    const void* attn_norm;   /* bf16 [hidden] */
+    const void* w_qkv;       /* nld_pack_qkv(Wq, Wk, Wv) */
+    const void* w_o;         /* nld_pack_linear(Wo [hidden][n_q_heads*head_dim]) */
+    const void* ffn_norm;    /* bf16 [hidden] */
+    const void* w_gate_up;   /* nld_pack_gate_up(Wg, Wu) */
+    const void* w_down;      /* nld_pack_linear(Wd [hidden][ffn]) */
+} nld_layer_weights;
+
+typedef struct {
+    const void* embed;                 /* bf16 [vocab][hidden], row-major (not packed) */
+    const void* final_norm;            /* bf16 [hidden] */
+    const void* lm_head;               /* nld_pack_linear(W_lm [vocab][hidden]) */
+    const nld_layer_weights* layers;   /* host array [n_layers]; copied by nld_model_create */
+} nld_weights;
+
+/* KV cache.  K and V of every layer, sequence and KV head, bf16:
+ *   k: [n_layers][batch][n_kv_heads][max_len][head_dim]
+ *   v: [n_layers][batch][n_kv_heads][max_len/64][head_dim][64]
+ *      (64-position tiles, each stored transposed: head_dim rows of 64 positions)
+ * lengths[b] = P_b, the committed length of sequence b.  Rows at positions
+ * >= P_b are scratch: a block pass (either mode) writes its own K/V rows to
+ * positions [P_b, P_b + k) and attends to them there, but only
+ * nld_verify_accept advances lengths (by L+1), which commits the anchor row
+ * and the accepted draft rows; the rest are overwritten by later passes. */
+typedef struct {
+    void* k;
+    void* v;
+    int32_t* lengths;   /* device int32 [batch] */
+    int32_t batch;
+    int32_t max_len;    /* multiple of 64 */
+} nld_kv_cache;
+
+typedef struct nld_model nld_model;   /* opaque handle; borrows the weight pointers */
+
+/* Message for the last non-OK status returned on this thread. */
+const char* nld_last_error(void);
+const char* nld_status_string(int32_t status);
+
+/* Validate `cfg` and the weight pointers (host-side only) and build a handle.
+ * Errors: INVALID_ARG (null pointer, non-positive size), SHAPE (hidden not a
+ * multiple of 32, head_dim not 64/128, n_q_heads not a multiple of
+ * n_kv_heads, ffn not a multiple of 8).  No device call is made. */
+nld_status nld_model_create(const nld_config* cfg, const nld_weights* w, nld_model** out);
+void nld_model_destroy(nld_model* m);
+
+/* ---- weight packing (one-time, on the device) ------------------------------
+ * Packed layout: the output features are cut into tiles of 16, the input
+ * features into steps of 32 (zero-padded); tile t, step s is one contiguous
+ * 1 KiB block whose 16-byte lane l holds W[16t + l%16][32s + 8(l/16) .. +8]
+ * -- one MFMA B-operand per wavefront load.  Sizes come from
+ * nld_packed_bytes.  Source matrices are bf16 row-major [out][in]; source and
+ * destination must not overlap. */
+#define NLD_PACK_LINEAR 0
+#define NLD_PACK_QKV 1       /* rows of each 16-column tile pair RoPE partners (i, i + head_dim/2) */
+#define NLD_PACK_GATE_UP 2   /* each 16-column tile holds 8 gate rows then the same 8 up rows */
+size_t nld_packed_bytes(int32_t kind, const nld_config* cfg, int32_t out_dim, int32_t in_dim);
+/* out_dim x in_dim matrix w.  Errors: INVALID_ARG, SHAPE (in_dim % 8 != 0). */
+nld_status nld_pack_linear(const void* w, int32_t out_dim, int32_t in_dim, void* packed, void* stream);
+/* wq [n_q_heads*head_dim][hidden], wk/wv [n_kv_heads*head_dim][hidden]. */
+nld_status nld_pack_qkv(const nld_config* cfg, const void* wq, const void* wk, const void* wv, void* packed,
+                        void* stream);
+/* wg, wu [ffn][hidden]. */
+nld_status nld_pack_gate_up(const nld_config* cfg, const void* wg, const void* wu, void* packed, void* stream);
+
+/* ---- workspace -------------------------------------------------------------
+ * Bytes of scratch one call with this batch, block size and cache capacity
+ * needs (activations, attention partials, argmax partials, counters, status
+ * word).  nld_workspace_init must run once on a new workspace before its
+ * first use (it clears the counters and the status word). */
+size_t nld_workspace_bytes(const nld_model* m, int32_t batch, int32_t k, int32_t max_len);
+nld_status nld_workspace_init(void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- the block-decode step ---------------------------------------------------
+ * One forward pass over tokens[batch][k] (block row j at position P_b + j):
+ * embedding -> n_layers x (RMSNorm, QKV, RoPE, K/V write to cache rows
+ * [P_b, P_b+k), block-masked GQA attention over the P_b + k keys, O + residual,
+ * RMSNorm, SwiGLU, down + residual) -> final RMSNorm -> LM head -> per-row
+ * argmax (lowest index among equal maxima).
+ * mode: NLD_MODE_VERIFY (block causal) or NLD_MODE_DRAFT (rows j >= bidir_from
+ * see every block column, rows below it are causal); bidir_from in [0, k].
+ * logits (optional) f32 [batch][k][vocab]; argmax (optional) int32 [batch][k].
+ * lengths are not changed.
+ * Errors: INVALID_ARG (null model/cache/tokens/workspace, batch < 1,
+ * k < 1 or k > 64, bad mode/bidir_from, kv->batch != batch), SHAPE
+ * (n_q_heads/n_kv_heads * k > 256), CAPACITY (ws_bytes too small). */
+nld_status nld_block_forward(const nld_model* m, const nld_kv_cache* kv, const int32_t* tokens, int32_t batch,
+                             int32_t k, int32_t mode, int32_t bidir_from, float* logits, int32_t* argmax,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* Diffusion draft (Sec. 3.3): runs the draft pass over [anchor[b], mask x (k-1)]
+ * and writes draft[b][j-1] = argmax of draft row j, j = 1..k-1 (k >= 2).
+ * logits optional as above.  Cache rows [P_b, P_b+k) are overwritten
+ * (scratch); lengths unchanged.  Errors as nld_block_forward. */
+nld_status nld_draft(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor, int32_t batch, int32_t k,
+                     int32_t bidir_from, int32_t* draft, float* logits, void* workspace, size_t ws_bytes,
+                     void* stream);
+
+/* AR verify + acceptance (Sec. 3.3): runs the causal pass over
+ * [anchor[b], draft[b][0..k-2]], takes a_j = argmax of verify row j, accepts
+ * L_b = the number of leading j in 1..k-1 with draft[b][j-1] == a_{j-1}, and
+ * writes accept_len[b] = L_b, committed[b][0..k) = d_1..d_{L_b}, a_{L_b},
+ * then -1 padding, next_anchor[b] = a_{L_b}, and lengths[b] += L_b + 1 (the
+ * anchor row and the accepted draft rows become committed cache rows).
+ * next_anchor may be the same buffer as anchor (it is written last), which
+ * keeps a decode loop on the device.
+ * With k = 1 this is one step of AR decoding (Sec. 3.1); draft may then be NULL.
+ * logits optional.  Errors as nld_block_forward. */
+nld_status nld_verify_accept(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor,
+                             const int32_t* draft, int32_t batch, int32_t k, int32_t* accept_len,
+                             int32_t* committed, int32_t* next_anchor, float* logits, void* workspace,
+                             size_t ws_bytes, void* stream);
+
+/* Argmax + acceptance alone, from given logits f32 [batch][k][vocab] and
+ * draft int32 [batch][k-1] (NULL when k = 1): writes argmax [batch][k] and the
+ * same accept_len / committed / next_anchor as nld_verify_accept.  Does not
+ * touch any cache.  workspace must be initialized and hold at least
+ * nld_accept_workspace_bytes(batch, k).  Errors: INVALID_ARG, CAPACITY. */
+size_t nld_accept_workspace_bytes(int32_t batch, int32_t k);
+nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int32_t batch, int32_t k,
+                                  int32_t vocab, int32_t* argmax, int32_t* accept_len, int32_t* committed,
+                                  int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- tracing aid -------------------------------------------------------------
+ * While enabled, every kernel launch made by the block-decode calls is
+ * bracketed by HIP events recorded on the call's stream (do not enable it
+ * while a stream is being captured into a graph).  nld_trace_read
+ * synchronizes on those events and returns, per kernel class, the summed
+ * milliseconds and the launch count since the last read (host arrays of
+ * length n >= NLD_TRACE_CLASSES), then clears the record. */
+#define NLD_TRACE_EMBED 0
+#define NLD_TRACE_QKV 1
+#define NLD_TRACE_ATTENTION 2
+#define NLD_TRACE_O_PROJ 3
+#define NLD_TRACE_GATE_UP 4
+#define NLD_TRACE_DOWN 5
+#define NLD_TRACE_LM_HEAD 6
+#define NLD_TRACE_ARGMAX 7
+#define NLD_TRACE_CLASSES 8
+nld_status nld_trace_enable(int32_t on);
+nld_status nld_trace_read(float* ms, int32_t* counts, int32_t n);
+
+/* Synchronizes `stream`, copies the sticky device status word to *host_bits
+ * (host pointer) and clears it.  Returns NLD_ERR_DEVICE if any bit was set. */
+nld_status nld_read_device_status(void* workspace, uint32_t* host_bits, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NLD_H */

@@ -1,0 +1,657 @@
+// C ABI of libnld: host-side validation, workspace layout and launch sequence of
+// the block-decode step (declared in include/nld.h).
+#include "../../include/nld.h"
+#include "nld_internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+using namespace nld;
+
+struct nld_model {
+    nld_config cfg;
+    nld_weights w;
+    std::vector<nld_layer_weights> layers;
+};
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+nld_status fail(nld_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+#define HIP_TRY(expr)                                                                              \
+    do {                                                                                           \
+        hipError_t e_ = (expr);                                                                    \
+        if (e_ != hipSuccess) return fail(NLD_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+// ---------------------------------------------------------------- tracing aid
+struct TraceRec {
+    int cls;
+    hipEvent_t start, stop;
+};
+bool g_trace_on = false;
+std::vector<TraceRec> g_trace;
+
+struct TraceScope {
+    TraceRec rec{};
+    hipStream_t s;
+    bool on;
+    TraceScope(int cls, hipStream_t st) : s(st), on(g_trace_on) {
+        if (!on) return;
+        rec.cls = cls;
+        if (hipEventCreate(&rec.start) != hipSuccess || hipEventCreate(&rec.stop) != hipSuccess) {
+            on = false;
+            return;
+        }
+        (void)hipEventRecord(rec.start, s);
+    }
+    ~TraceScope() {
+        if (!on) return;
+        (void)hipEventRecord(rec.stop, s);
+        g_trace.push_back(rec);
+    }
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+int env_int(const char* name, int dflt) {
+    const char* v = getenv(name);
+    return (v && *v) ? atoi(v) : dflt;
+}
+
+// ---------------------------------------------------------------- workspace layout
+struct Layout {
+    int M, Mpad, units, n_splits, chunk, attn_waves, rows_pad, lm_tiles, h_tiles, groups;
+    size_t status, ctr_resid0, ctr_resid1, ctr_attn, ctr_fin, ctr_end;
+    size_t x, xg, inv_a, inv_f, part_ss, q, o, act, keys, amax, po, pml, total;
+};
+
+Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
+    Layout L{};
+    L.M = batch * k;
+    L.Mpad = cdiv(L.M, 64) * 64;
+    L.groups = L.Mpad / 16;
+    L.units = batch * c.n_kv_heads;
+    const int G = c.n_q_heads / c.n_kv_heads;
+    L.attn_waves = cdiv(G * k, 16);
+    L.rows_pad = L.attn_waves * 16;
+    L.lm_tiles = cdiv(c.vocab, 16);
+    L.h_tiles = c.hidden / 16;
+    // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
+    const int target = env_int("NLD_ATTN_TARGET_WG", 256);
+    int ns = cdiv(target, L.units);
+    const int max_splits = cdiv(max_len, 64);
+    if (ns > max_splits) ns = max_splits;
+    if (ns < 1) ns = 1;
+    L.chunk = cdiv(cdiv(max_len, ns), 64) * 64;
+    L.n_splits = cdiv(max_len, L.chunk);
+
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = align256(off + bytes);
+        return o;
+    };
+    L.status = take(4);
+    L.ctr_resid0 = take(4 * (size_t)L.groups);
+    L.ctr_resid1 = take(4 * (size_t)L.groups);
+    L.ctr_attn = take(4 * (size_t)L.units);
+    L.ctr_fin = take(4 * (size_t)batch);
+    L.ctr_end = off;
+    const size_t H = c.hidden, QD = (size_t)c.n_q_heads * c.head_dim;
+    L.x = take(4 * L.Mpad * H);
+    L.xg = take(2 * L.Mpad * H);
+    L.inv_a = take(4 * (size_t)L.Mpad);
+    L.inv_f = take(4 * (size_t)L.Mpad);
+    L.part_ss = take(4 * L.Mpad * (size_t)L.h_tiles);
+    L.q = take(2 * L.Mpad * QD);
+    L.o = take(2 * L.Mpad * QD);
+    L.act = take(2 * L.Mpad * (size_t)c.ffn);
+    L.keys = take(8 * L.Mpad * (size_t)L.lm_tiles);
+    L.amax = take(4 * (size_t)L.Mpad);
+    L.po = take(4 * (size_t)L.units * L.n_splits * L.rows_pad * c.head_dim);
+    L.pml = take(4 * 2 * (size_t)L.units * L.n_splits * L.rows_pad);
+    L.total = off;
+    return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
+
+nld_status check_config(const nld_config* c) {
+    if (!c) return fail(NLD_ERR_INVALID_ARG, "config is NULL");
+    if (c->n_layers < 1 || c->hidden < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn < 1 || c->vocab < 1)
+        return fail(NLD_ERR_INVALID_ARG, "config sizes must be positive");
+    if (c->hidden % 32) return fail(NLD_ERR_SHAPE, "hidden (%d) must be a multiple of 32", c->hidden);
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(NLD_ERR_SHAPE, "head_dim must be 64 or 128");
+    if (c->n_q_heads % c->n_kv_heads) return fail(NLD_ERR_SHAPE, "n_q_heads must be a multiple of n_kv_heads");
+    if (c->ffn % 8) return fail(NLD_ERR_SHAPE, "ffn (%d) must be a multiple of 8", c->ffn);
+    if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab)
+        return fail(NLD_ERR_INVALID_ARG, "mask_token_id outside [0, vocab)");
+    if (!(c->rope_base > 1.0f) || !(c->rms_eps >= 0.0f)) return fail(NLD_ERR_INVALID_ARG, "bad rope_base or rms_eps");
+    return NLD_OK;
+}
+
+// ---------------------------------------------------------------- GEMM launch plan
+struct GemmPlan {
+    int mt, ct, nw, gx, gy;
+};
+
+GemmPlan plan_gemm(int epi, int M, int n_tiles) {
+    GemmPlan p;
+    p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    p.gy = cdiv(M, 16 * p.mt);
+    if (epi == EPI_LMHEAD) {
+        p.ct = 4;
+        p.nw = 4;
+    } else if (epi == EPI_SWIGLU) {
+        p.ct = 2;
+        p.nw = 8;
+    } else {
+        p.ct = 1;
+        p.nw = 8;
+    }
+    p.gx = cdiv(n_tiles, p.ct);
+    return p;
+}
+
+hipError_t gemm(int epi, const GemmArgs& a, hipStream_t s) {
+    const GemmPlan p = plan_gemm(epi, a.M, a.n_tiles);
+    return launch_gemm(epi, p.mt, p.ct, p.nw, p.gx, p.gy, a, s);
+}
+
+enum Source { SRC_TOKENS = 0, SRC_DRAFT = 1, SRC_VERIFY = 2 };
+
+struct PassIO {
+    int source;
+    const int32_t* tokens;
+    const int32_t* anchor;
+    const int32_t* draft_in;
+    int mode, bidir_from;
+    float* logits;
+    int32_t* argmax_out;
+    int finish;
+    int32_t* draft_out;
+    int32_t* accept_len;
+    int32_t* committed;
+    int32_t* next_anchor;
+    bool advance_lengths;
+};
+
+nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, int k, void* ws, size_t ws_bytes,
+                         Layout* out) {
+    if (!m) return fail(NLD_ERR_INVALID_ARG, "model is NULL");
+    if (!kv || !kv->k || !kv->v || !kv->lengths) return fail(NLD_ERR_INVALID_ARG, "kv cache or one of its pointers is NULL");
+    if (!ws) return fail(NLD_ERR_INVALID_ARG, "workspace is NULL");
+    if (batch < 1) return fail(NLD_ERR_INVALID_ARG, "batch must be >= 1");
+    if (kv->batch != batch) return fail(NLD_ERR_INVALID_ARG, "kv->batch (%d) != batch (%d)", kv->batch, batch);
+    if (k < 1 || k > 64) return fail(NLD_ERR_INVALID_ARG, "k must be in [1, 64] (got %d)", k);
+    if (kv->max_len < 64 || kv->max_len % 64) return fail(NLD_ERR_INVALID_ARG, "max_len must be a positive multiple of 64");
+    const nld_config& c = m->cfg;
+    const int G = c.n_q_heads / c.n_kv_heads;
+    if (G * k > 256) return fail(NLD_ERR_SHAPE, "(n_q_heads/n_kv_heads)*k = %d exceeds 256", G * k);
+    *out = make_layout(c, batch, k, kv->max_len);
+    if (ws_bytes < out->total)
+        return fail(NLD_ERR_CAPACITY, "workspace holds %zu bytes, this call needs %zu", ws_bytes, out->total);
+    return NLD_OK;
+}
+
+nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int k, const PassIO& io, void* ws,
+                    const Layout& L, hipStream_t s) {
+    const nld_config& c = mdl->cfg;
+    const int M = L.M;
+    const int D = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
+    const size_t kv_layer = (size_t)batch * nkv * kv->max_len * D;
+    uint32_t* status = at<uint32_t>(ws, L.status);
+    float* x = at<float>(ws, L.x);
+    uint16_t* xg = at<uint16_t>(ws, L.xg);
+    float* inv_a = at<float>(ws, L.inv_a);
+    float* inv_f = at<float>(ws, L.inv_f);
+
+    EmbedArgs e{};
+    e.tokens = io.tokens;
+    e.anchor = io.anchor;
+    e.draft = io.draft_in;
+    e.source = io.source;
+    e.k_blk = k;
+    e.M = M;
+    e.mask_id = c.mask_token_id;
+    e.vocab = c.vocab;
+    e.hidden = c.hidden;
+    e.embed = (const uint16_t*)mdl->w.embed;
+    e.gain = (const uint16_t*)mdl->layers[0].attn_norm;
+    e.eps = c.rms_eps;
+    e.x = x;
+    e.xg = xg;
+    e.inv_rms = inv_a;
+    e.status = status;
+    {
+        TraceScope ts(NLD_TRACE_EMBED, s);
+        HIP_TRY(launch_embed(e, s));
+    }
+
+    const int ks_h = cdiv(c.hidden, 32), ks_q = cdiv(nq * D, 32), ks_f = cdiv(c.ffn, 32);
+    for (int l = 0; l < c.n_layers; ++l) {
+        const nld_layer_weights& W = mdl->layers[l];
+        uint16_t* kc = (uint16_t*)kv->k + (size_t)l * kv_layer;
+        uint16_t* vc = (uint16_t*)kv->v + (size_t)l * kv_layer;
+
+        GemmArgs g{};
+        g.A = xg;
+        g.lda = c.hidden;
+        g.M = M;
+        g.K = c.hidden;
+        g.W = (const uint4*)W.w_qkv;
+        g.n_tiles = (nq + 2 * nkv) * D / 16;
+        g.ksteps = ks_h;
+        g.inv_rms = inv_a;
+        g.q_out = at<uint16_t>(ws, L.q);
+        g.kc = kc;
+        g.vc = vc;
+        g.lengths = kv->lengths;
+        g.k_blk = k;
+        g.n_q_heads = nq;
+        g.n_kv_heads = nkv;
+        g.head_dim = D;
+        g.max_len = kv->max_len;
+        g.log2_base = log2((double)c.rope_base);
+        g.status = status;
+        {
+            TraceScope ts(NLD_TRACE_QKV, s);
+            HIP_TRY(gemm(EPI_QKV, g, s));
+        }
+
+        AttnArgs at_{};
+        at_.q = at<uint16_t>(ws, L.q);
+        at_.kc = kc;
+        at_.vc = vc;
+        at_.lengths = kv->lengths;
+        at_.o = at<uint16_t>(ws, L.o);
+        at_.part_o = at<float>(ws, L.po);
+        at_.part_ml = at<float>(ws, L.pml);
+        at_.counters = at<uint32_t>(ws, L.ctr_attn);
+        at_.k_blk = k;
+        at_.n_q_heads = nq;
+        at_.n_kv_heads = nkv;
+        at_.max_len = kv->max_len;
+        at_.n_splits = L.n_splits;
+        at_.chunk = L.chunk;
+        at_.mode = io.mode;
+        at_.bidir_from = io.bidir_from;
+        at_.rows_pad = L.rows_pad;
+        at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+        {
+            TraceScope ts(NLD_TRACE_ATTENTION, s);
+            HIP_TRY(launch_attention(D, L.attn_waves, L.units, at_, s));
+        }
+
+        GemmArgs go{};
+        go.A = at<uint16_t>(ws, L.o);
+        go.lda = nq * D;
+        go.M = M;
+        go.K = nq * D;
+        go.W = (const uint4*)W.w_o;
+        go.n_tiles = L.h_tiles;
+        go.ksteps = ks_q;
+        go.x = x;
+        go.xg = xg;
+        go.gain = (const uint16_t*)W.ffn_norm;
+        go.part_ss = at<float>(ws, L.part_ss);
+        go.inv_rms_out = inv_f;
+        go.counters = at<uint32_t>(ws, L.ctr_resid0);
+        go.eps = c.rms_eps;
+        {
+            TraceScope ts(NLD_TRACE_O_PROJ, s);
+            HIP_TRY(gemm(EPI_RESID, go, s));
+        }
+
+        GemmArgs gu{};
+        gu.A = xg;
+        gu.lda = c.hidden;
+        gu.M = M;
+        gu.K = c.hidden;
+        gu.W = (const uint4*)W.w_gate_up;
+        gu.n_tiles = cdiv(c.ffn, 8);
+        gu.ksteps = ks_h;
+        gu.inv_rms = inv_f;
+        gu.act = at<uint16_t>(ws, L.act);
+        gu.ffn = c.ffn;
+        {
+            TraceScope ts(NLD_TRACE_GATE_UP, s);
+            HIP_TRY(gemm(EPI_SWIGLU, gu, s));
+        }
+
+        GemmArgs gd{};
+        gd.A = at<uint16_t>(ws, L.act);
+        gd.lda = c.ffn;
+        gd.M = M;
+        gd.K = c.ffn;
+        gd.W = (const uint4*)W.w_down;
+        gd.n_tiles = L.h_tiles;
+        gd.ksteps = ks_f;
+        gd.x = x;
+        gd.xg = xg;
+        gd.gain = (const uint16_t*)(l + 1 < c.n_layers ? mdl->layers[l + 1].attn_norm : mdl->w.final_norm);
+        gd.part_ss = at<float>(ws, L.part_ss);
+        gd.inv_rms_out = inv_a;
+        gd.counters = at<uint32_t>(ws, L.ctr_resid1);
+        gd.eps = c.rms_eps;
+        {
+            TraceScope ts(NLD_TRACE_DOWN, s);
+            HIP_TRY(gemm(EPI_RESID, gd, s));
+        }
+    }
+
+    GemmArgs gl{};
+    gl.A = xg;
+    gl.lda = c.hidden;
+    gl.M = M;
+    gl.K = c.hidden;
+    gl.W = (const uint4*)mdl->w.lm_head;
+    gl.n_tiles = L.lm_tiles;
+    gl.ksteps = ks_h;
+    gl.inv_rms = inv_a;
+    gl.logits = io.logits;
+    gl.part_keys = at<unsigned long long>(ws, L.keys);
+    gl.vocab = c.vocab;
+    {
+        TraceScope ts(NLD_TRACE_LM_HEAD, s);
+        HIP_TRY(gemm(EPI_LMHEAD, gl, s));
+    }
+
+    ArgmaxArgs am{};
+    am.part_keys = at<unsigned long long>(ws, L.keys);
+    am.n_tiles = L.lm_tiles;
+    am.vocab = c.vocab;
+    am.M = M;
+    am.k_blk = k;
+    am.batch = batch;
+    am.argmax_ws = at<int32_t>(ws, L.amax);
+    am.argmax_out = io.argmax_out;
+    am.finish = io.finish;
+    am.draft_in = io.draft_in;
+    am.draft_out = io.draft_out;
+    am.accept_len = io.accept_len;
+    am.committed = io.committed;
+    am.next_anchor = io.next_anchor;
+    am.lengths = io.advance_lengths ? kv->lengths : nullptr;
+    am.counters = at<uint32_t>(ws, L.ctr_fin);
+    {
+        TraceScope ts(NLD_TRACE_ARGMAX, s);
+        HIP_TRY(launch_argmax_finish(am, s));
+    }
+    return NLD_OK;
+}
+
+}  // namespace
+
+// =====================================================================================
+extern "C" {
+
+const char* nld_last_error(void) { return g_err; }
+
+const char* nld_status_string(int32_t st) {
+    switch (st) {
+        case NLD_OK: return "ok";
+        case NLD_ERR_INVALID_ARG: return "invalid argument";
+        case NLD_ERR_SHAPE: return "unsupported shape";
+        case NLD_ERR_CAPACITY: return "workspace too small";
+        case NLD_ERR_HIP: return "HIP runtime error";
+        case NLD_ERR_UNSUPPORTED: return "unsupported";
+        case NLD_ERR_DEVICE: return "device-side error";
+        default: return "unknown status";
+    }
+}
+
+nld_status nld_model_create(const nld_config* cfg, const nld_weights* w, nld_model** out) {
+    if (!out) return fail(NLD_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    nld_status st = check_config(cfg);
+    if (st != NLD_OK) return st;
+    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
+        return fail(NLD_ERR_INVALID_ARG, "a model-level weight pointer is NULL");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const nld_layer_weights& L = w->layers[l];
+        if (!L.attn_norm || !L.w_qkv || !L.w_o || !L.ffn_norm || !L.w_gate_up || !L.w_down)
+            return fail(NLD_ERR_INVALID_ARG, "a weight pointer of layer %d is NULL", l);
+    }
+    nld_model* m = new nld_model;
+    m->cfg = *cfg;
+    m->w = *w;
+    m->layers.assign(w->layers, w->layers + cfg->n_layers);
+    m->w.layers = m->layers.data();
+    *out = m;
+    return NLD_OK;
+}
+
+void nld_model_destroy(nld_model* m) { delete m; }
+
+size_t nld_packed_bytes(int32_t kind, const nld_config* cfg, int32_t out_dim, int32_t in_dim) {
+    if (in_dim < 1 || out_dim < 1) return 0;
+    int tiles;
+    if (kind == NLD_PACK_GATE_UP) tiles = cdiv(out_dim, 8);            // out_dim = ffn
+    else if (kind == NLD_PACK_QKV) {
+        if (!cfg) return 0;
+        tiles = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim / 16;
+    } else tiles = cdiv(out_dim, 16);
+    return (size_t)tiles * cdiv(in_dim, 32) * 1024;
+}
+
+nld_status nld_pack_linear(const void* w, int32_t out_dim, int32_t in_dim, void* packed, void* stream) {
+    if (!w || !packed) return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    if (out_dim < 1 || in_dim < 1) return fail(NLD_ERR_INVALID_ARG, "sizes must be positive");
+    if (in_dim % 8) return fail(NLD_ERR_SHAPE, "in_dim (%d) must be a multiple of 8", in_dim);
+    PackArgs p{};
+    p.src0 = (const uint16_t*)w;
+    p.kind = PACK_LINEAR;
+    p.out_dim = out_dim;
+    p.in_dim = in_dim;
+    p.n_tiles = cdiv(out_dim, 16);
+    p.ksteps = cdiv(in_dim, 32);
+    p.dst = (uint4*)packed;
+    HIP_TRY(launch_pack(p, (hipStream_t)stream));
+    return NLD_OK;
+}
+
+nld_status nld_pack_qkv(const nld_config* cfg, const void* wq, const void* wk, const void* wv, void* packed,
+                        void* stream) {
+    nld_status st = check_config(cfg);
+    if (st != NLD_OK) return st;
+    if (!wq || !wk || !wv || !packed) return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    PackArgs p{};
+    p.src0 = (const uint16_t*)wq;
+    p.src1 = (const uint16_t*)wk;
+    p.src2 = (const uint16_t*)wv;
+    p.kind = PACK_QKV;
+    p.head_dim = cfg->head_dim;
+    p.rows0 = cfg->n_q_heads * cfg->head_dim;
+    p.rows1 = cfg->n_kv_heads * cfg->head_dim;
+    p.out_dim = p.rows0 + 2 * p.rows1;
+    p.in_dim = cfg->hidden;
+    p.n_tiles = p.out_dim / 16;
+    p.ksteps = cdiv(cfg->hidden, 32);
+    p.dst = (uint4*)packed;
+    HIP_TRY(launch_pack(p, (hipStream_t)stream));
+    return NLD_OK;
+}
+
+nld_status nld_pack_gate_up(const nld_config* cfg, const void* wg, const void* wu, void* packed, void* stream) {
+    nld_status st = check_config(cfg);
+    if (st != NLD_OK) return st;
+    if (!wg || !wu || !packed) return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    PackArgs p{};
+    p.src0 = (const uint16_t*)wg;
+    p.src1 = (const uint16_t*)wu;
+    p.kind = PACK_GATE_UP;
+    p.rows0 = cfg->ffn;
+    p.out_dim = 2 * cfg->ffn;
+    p.in_dim = cfg->hidden;
+    p.n_tiles = cdiv(cfg->ffn, 8);
+    p.ksteps = cdiv(cfg->hidden, 32);
+    p.dst = (uint4*)packed;
+    HIP_TRY(launch_pack(p, (hipStream_t)stream));
+    return NLD_OK;
+}
+
+size_t nld_workspace_bytes(const nld_model* m, int32_t batch, int32_t k, int32_t max_len) {
+    if (!m || batch < 1 || k < 1 || max_len < 64) return 0;
+    return make_layout(m->cfg, batch, k, max_len).total;
+}
+
+nld_status nld_workspace_init(void* workspace, size_t ws_bytes, void* stream) {
+    if (!workspace) return fail(NLD_ERR_INVALID_ARG, "workspace is NULL");
+    if (ws_bytes < 256) return fail(NLD_ERR_CAPACITY, "workspace too small");
+    HIP_TRY(launch_fill_zero(workspace, ws_bytes & ~(size_t)3, (hipStream_t)stream));
+    return NLD_OK;
+}
+
+nld_status nld_block_forward(const nld_model* m, const nld_kv_cache* kv, const int32_t* tokens, int32_t batch,
+                             int32_t k, int32_t mode, int32_t bidir_from, float* logits, int32_t* argmax,
+                             void* workspace, size_t ws_bytes, void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (!tokens) return fail(NLD_ERR_INVALID_ARG, "tokens is NULL");
+    if (mode != NLD_MODE_VERIFY && mode != NLD_MODE_DRAFT) return fail(NLD_ERR_INVALID_ARG, "mode must be 0 or 1");
+    if (bidir_from < 0 || bidir_from > k) return fail(NLD_ERR_INVALID_ARG, "bidir_from must be in [0, k]");
+    PassIO io{};
+    io.source = SRC_TOKENS;
+    io.tokens = tokens;
+    io.mode = mode;
+    io.bidir_from = bidir_from;
+    io.logits = logits;
+    io.argmax_out = argmax;
+    io.finish = FINISH_NONE;
+    return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+nld_status nld_draft(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor, int32_t batch, int32_t k,
+                     int32_t bidir_from, int32_t* draft, float* logits, void* workspace, size_t ws_bytes,
+                     void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (k < 2) return fail(NLD_ERR_INVALID_ARG, "a draft needs k >= 2");
+    if (!anchor || !draft) return fail(NLD_ERR_INVALID_ARG, "anchor or draft is NULL");
+    if (bidir_from < 0 || bidir_from > k) return fail(NLD_ERR_INVALID_ARG, "bidir_from must be in [0, k]");
+    PassIO io{};
+    io.source = SRC_DRAFT;
+    io.anchor = anchor;
+    io.mode = NLD_MODE_DRAFT;
+    io.bidir_from = bidir_from;
+    io.logits = logits;
+    io.finish = FINISH_DRAFT;
+    io.draft_out = draft;
+    return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+nld_status nld_verify_accept(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor,
+                             const int32_t* draft, int32_t batch, int32_t k, int32_t* accept_len,
+                             int32_t* committed, int32_t* next_anchor, float* logits, void* workspace,
+                             size_t ws_bytes, void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (!anchor || !accept_len || !committed || !next_anchor)
+        return fail(NLD_ERR_INVALID_ARG, "anchor, accept_len, committed or next_anchor is NULL");
+    if (k > 1 && !draft) return fail(NLD_ERR_INVALID_ARG, "draft is NULL");
+    PassIO io{};
+    io.source = SRC_VERIFY;
+    io.anchor = anchor;
+    io.draft_in = draft;
+    io.mode = NLD_MODE_VERIFY;
+    io.logits = logits;
+    io.finish = FINISH_ACCEPT;
+    io.accept_len = accept_len;
+    io.committed = committed;
+    io.next_anchor = next_anchor;
+    io.advance_lengths = true;
+    return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+size_t nld_accept_workspace_bytes(int32_t batch, int32_t k) {
+    if (batch < 1 || k < 1) return 0;
+    return align256(4) + align256(4 * (size_t)batch) + align256(4 * (size_t)batch * k);
+}
+
+nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int32_t batch, int32_t k,
+                                  int32_t vocab, int32_t* argmax, int32_t* accept_len, int32_t* committed,
+                                  int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream) {
+    if (!logits || !argmax || !accept_len || !committed || !next_anchor || !workspace)
+        return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    if (batch < 1 || k < 1 || k > 64 || vocab < 1) return fail(NLD_ERR_INVALID_ARG, "bad batch, k or vocab");
+    if (k > 1 && !draft) return fail(NLD_ERR_INVALID_ARG, "draft is NULL");
+    if (ws_bytes < nld_accept_workspace_bytes(batch, k)) return fail(NLD_ERR_CAPACITY, "workspace too small");
+    ArgmaxArgs am{};
+    am.part_keys = nullptr;
+    am.logits = logits;
+    am.vocab = vocab;
+    am.M = batch * k;
+    am.k_blk = k;
+    am.batch = batch;
+    am.counters = (uint32_t*)((char*)workspace + align256(4));
+    am.argmax_ws = (int32_t*)((char*)workspace + align256(4) + align256(4 * (size_t)batch));
+    am.argmax_out = argmax;
+    am.finish = FINISH_ACCEPT;
+    am.draft_in = draft;
+    am.accept_len = accept_len;
+    am.committed = committed;
+    am.next_anchor = next_anchor;
+    HIP_TRY(launch_argmax_finish(am, (hipStream_t)stream));
+    return NLD_OK;
+}
+
+nld_status nld_trace_enable(int32_t on) {
+    g_trace_on = on != 0;
+    return NLD_OK;
+}
+
+nld_status nld_trace_read(float* ms, int32_t* counts, int32_t n) {
+    if (!ms || !counts || n < NLD_TRACE_CLASSES) return fail(NLD_ERR_INVALID_ARG, "need host arrays of NLD_TRACE_CLASSES");
+    for (int i = 0; i < n; ++i) {
+        ms[i] = 0.f;
+        counts[i] = 0;
+    }
+    nld_status st = NLD_OK;
+    for (TraceRec& r : g_trace) {
+        float t = 0.f;
+        if (st == NLD_OK) {
+            hipError_t e = hipEventSynchronize(r.stop);
+            if (e == hipSuccess) e = hipEventElapsedTime(&t, r.start, r.stop);
+            if (e != hipSuccess) st = fail(NLD_ERR_HIP, "trace event: %s", hipGetErrorString(e));
+        }
+        ms[r.cls] += t;
+        counts[r.cls] += 1;
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+    }
+    g_trace.clear();
+    return st;
+}
+
+nld_status nld_read_device_status(void* workspace, uint32_t* host_bits, void* stream) {
+    if (!workspace || !host_bits) return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(hipMemcpy(host_bits, workspace, 4, hipMemcpyDeviceToHost));
+    HIP_TRY(launch_fill_zero(workspace, 4, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (*host_bits) return fail(NLD_ERR_DEVICE, "device status bits 0x%x", *host_bits);
+    return NLD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,151 @@
+// Internal declarations shared by the kernels and the host API of libnld.
+// gfx950 (CDNA4) only: 64-wide wavefronts, v_mfma_f32_16x16x32_bf16.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace nld {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+// ---------------------------------------------------------------- numerics helpers
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// float -> bfloat16, round to nearest even (finite inputs)
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// C[16x16] += A[16x32] * B[32x16].  Lane l supplies A[l%16][8(l/16)..+8] and
+// B[8(l/16)..+8][l%16] (8 bf16 each, one 16-byte register quad) and holds
+// C[4(l/16)+i][l%16], i = 0..3.
+__device__ __forceinline__ f32x4_t mfma_16x16x32(uint4 a, uint4 b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+}
+
+// Order-preserving key for a float value at column n: larger value wins, then
+// lower column.  -0.0 is folded onto +0.0 so that equal values tie on index.
+__device__ __forceinline__ unsigned long long argmax_key(float v, uint32_t n) {
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7FFFFFFFu) == 0u) u = 0u;
+    uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((unsigned long long)ord << 32) | (unsigned long long)(0xFFFFFFFFu - n);
+}
+__device__ __forceinline__ int32_t argmax_key_index(unsigned long long key) {
+    return (int32_t)(0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull));
+}
+
+// ---------------------------------------------------------------- kernel arguments
+enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
+
+struct GemmArgs {
+    // operands
+    const uint16_t* A;   // bf16 activations [M][lda], row-major
+    int lda;
+    int M;               // rows
+    int K;               // logical reduction length (multiple of 8)
+    const uint4* W;      // packed weights: [n_tiles][ksteps][64 lanes] x 16 bytes
+    int n_tiles;
+    int ksteps;          // ceil(K / 32)
+    const float* inv_rms;  // per-row RMSNorm scale applied to the product (QKV, SWIGLU, LMHEAD)
+    // EPI_RESID: x += A W^T; xg = bf16(x * gain); row sums of squares -> inv_rms_out
+    float* x;
+    uint16_t* xg;
+    const uint16_t* gain;
+    float* part_ss;      // [Mpad][n_tiles]
+    float* inv_rms_out;  // [Mpad]
+    uint32_t* counters;  // one per row group (blockIdx.y)
+    float eps;
+    // EPI_QKV
+    uint16_t* q_out;     // bf16 [M][n_q_heads * head_dim]
+    uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
+    uint16_t* vc;        // this layer's V cache [batch][n_kv_heads][max_len/64][head_dim][64]
+    const int32_t* lengths;
+    int k_blk;
+    int n_q_heads, n_kv_heads, head_dim, max_len;
+    double log2_base;
+    uint32_t* status;
+    // EPI_SWIGLU
+    uint16_t* act;       // bf16 [M][ffn]
+    int ffn;
+    // EPI_LMHEAD
+    float* logits;       // optional f32 [M][vocab]
+    unsigned long long* part_keys;  // [Mpad][n_tiles]
+    int vocab;
+};
+
+struct AttnArgs {
+    const uint16_t* q;   // bf16 [M][n_q_heads * D]
+    const uint16_t* kc;  // this layer's K cache
+    const uint16_t* vc;  // this layer's V cache (64-position transposed tiles)
+    const int32_t* lengths;
+    uint16_t* o;         // bf16 [M][n_q_heads * D]
+    float* part_o;       // [units][n_splits][rows_pad][D]
+    float* part_ml;      // [units][n_splits][rows_pad][2]
+    uint32_t* counters;  // [units]
+    int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
+    float scale_log2;    // log2(e) / sqrt(D)
+};
+
+struct EmbedArgs {
+    const int32_t* tokens;  // source 0: [batch][k]
+    const int32_t* anchor;  // sources 1, 2: [batch]
+    const int32_t* draft;   // source 2: [batch][k-1]
+    int source;             // 0 tokens, 1 draft block, 2 verify block
+    int k_blk, M, mask_id, vocab, hidden;
+    const uint16_t* embed;
+    const uint16_t* gain;
+    float eps;
+    float* x;
+    uint16_t* xg;
+    float* inv_rms;
+    uint32_t* status;
+};
+
+enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2 };
+
+struct ArgmaxArgs {
+    const unsigned long long* part_keys;  // [Mpad][n_tiles] (or NULL when reducing logits)
+    int n_tiles;
+    const float* logits;                  // [M][vocab] (used when part_keys is NULL)
+    int vocab;
+    int M, k_blk, batch;
+    int32_t* argmax_ws;                   // [M]
+    int32_t* argmax_out;                  // optional [M]
+    int finish;
+    const int32_t* draft_in;              // FINISH_ACCEPT: [batch][k-1]
+    int32_t* draft_out;                   // FINISH_DRAFT: [batch][k-1]
+    int32_t* accept_len;
+    int32_t* committed;                   // [batch][k]
+    int32_t* next_anchor;
+    int32_t* lengths;                     // advanced by L+1 (may be NULL)
+    uint32_t* counters;                   // [batch]
+};
+
+enum PackKind { PACK_LINEAR = 0, PACK_QKV = 1, PACK_GATE_UP = 2 };
+
+struct PackArgs {
+    const uint16_t* src0;
+    const uint16_t* src1;
+    const uint16_t* src2;
+    int kind;
+    int out_dim, in_dim, n_tiles, ksteps;
+    int head_dim, rows0, rows1;  // QKV: rows of wq and wk; GATE_UP: ffn in rows0
+    uint4* dst;
+};
+
+// ---------------------------------------------------------------- launchers (kernels.hip)
+hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_gemm(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a, hipStream_t s);
+hipError_t launch_attention(int head_dim, int waves, int units, const AttnArgs& a, hipStream_t s);
+hipError_t launch_argmax_finish(const ArgmaxArgs& a, hipStream_t s);
+
+}  // namespace nld

@@ -1,0 +1,284 @@
+"""GPU parity of the block-decode step against the CPU oracle, through the C ABI.
+
+Bar: logits within 2e-2 normwise relative error of the fp32 oracle; argmax and
+acceptance bit-exact on identical logits; integer-exact where every value is an
+exactly representable small integer.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import nld_oracle as O
+from synth.workloads import LazyWeights, ModelShape, SHAPE_TINY, WORKLOADS, tokens as synth_tokens, prefix_kv
+
+from gpu_common import (ArraySource, BF16_ONE, check_argmax, int_to_bf16_bits, log, rel_err)
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def R():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_05722_amd import runtime
+    return runtime
+
+
+# ----------------------------------------------------------------------------- integer-exact pins
+def _int_model(shape: ModelShape, seed: int, wv_int=False, lm_range=8):
+    """Zero layer weights (so the residual stream is the embedding), embeddings of +-1, gains 1,
+    small-integer LM head (and optionally small-integer Wv)."""
+    h = shape.hidden
+    zero = lambda o, i: np.zeros((o, i), dtype=np.uint16)
+    sign = synth.uniform_int(seed, "int.embed", (shape.vocab, h), 0, 1)
+    embed = np.where(sign == 1, BF16_ONE, np.uint16(0xBF80)).astype(np.uint16)
+    lm = int_to_bf16_bits(synth.uniform_int(seed, "int.lm", (shape.vocab, h), -lm_range, lm_range))
+    layers = []
+    for l in range(shape.n_layers):
+        wv = int_to_bf16_bits(synth.uniform_int(seed, "int.wv%d" % l, (shape.kv_dim, h), -1, 1)) if wv_int \
+            else zero(shape.kv_dim, h)
+        layers.append({"attn_norm": synth.bf16_ones(h), "wq": zero(shape.q_dim, h), "wk": zero(shape.kv_dim, h),
+                       "wv": wv, "wo": zero(h, shape.q_dim), "ffn_norm": synth.bf16_ones(h),
+                       "w_gate": zero(shape.ffn, h), "w_up": zero(shape.ffn, h), "w_down": zero(h, shape.ffn)})
+    return ArraySource(layers, embed, lm, synth.bf16_ones(h))
+
+
+INT_SHAPE = ModelShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=96, vocab=1000,
+                       rms_eps=0.0)
+
+
+@pytest.mark.parametrize("k", [1, 8, 40])
+def test_lm_head_integer_exact(R, k):
+    """Embedding gather, LM-head packing/tiling (ragged vocab 1000) and the fused argmax: the logits are
+    exact integers on both sides, so they must agree bit for bit, ties included (lowest index wins)."""
+    shape, seed = INT_SHAPE, 21
+    src = _int_model(shape, seed)
+    tok = synth_tokens(shape, seed, "int.tokens", (2, k))
+    w = O.OracleWeights(shape, src, np.float64)
+    kv = O.OracleKV(shape, 2, 64, np.float64)
+    ref, _, _ = O.block_forward(w, kv, tok, O.VERIFY)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, 2, 64)
+    ws = R.Workspace(model, 2, k, 64)
+    logits, am = R.block_forward(model, cache, ws, torch.from_numpy(tok).cuda(), R.VERIFY)
+    g = logits.cpu().numpy()
+    assert np.array_equal(g, ref.astype(np.float32)), "max diff %g" % np.max(np.abs(g - ref))
+    assert np.array_equal(am.cpu().numpy(), O.argmax_first(ref))
+    assert R.read_device_status(ws) == 0
+
+
+@pytest.mark.parametrize("prefix", [0, 5, 61])
+def test_qkv_value_rows_integer_exact(R, prefix):
+    """QKV packing, the V cache's transposed 64-position tiles and the cache row addressing: with +-1
+    activations and {-1,0,1} Wv the block's V rows are exact integers; K rows are zero."""
+    shape, seed, k = INT_SHAPE, 22, 8
+    src = _int_model(shape, seed, wv_int=True)
+    tok = synth_tokens(shape, seed, "int.tokens", (1, k))
+    w = O.OracleWeights(shape, src, np.float64)
+    kv = O.OracleKV(shape, 1, 128, np.float64)
+    kv.lengths[:] = prefix
+    _, nk, nv = O.block_forward(w, kv, tok, O.VERIFY)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, 1, 128)
+    cache.set_lengths([prefix])
+    ws = R.Workspace(model, 1, k, 128)
+    R.block_forward(model, cache, ws, torch.from_numpy(tok).cuda(), R.VERIFY, want_logits=False)
+    kg, vg = cache.read_kv(0, prefix, prefix + k)
+    f = lambda bits: O.bf16_bits_to_float(bits, np.float64)
+    assert np.array_equal(f(vg), nv[0]), "V rows differ"
+    assert np.array_equal(f(kg), nk[0])
+    assert int(cache.lengths.cpu()[0]) == prefix        # a block pass never commits
+
+
+# ----------------------------------------------------------------------------- argmax + acceptance
+def test_accept_from_logits_bit_exact(R):
+    """Argmax and longest-prefix acceptance on identical (oracle-side) logits, with planted exact ties,
+    signed zeros and drafts planted to give every acceptance length 0..k-1."""
+    B, k, V = 9, 8, 5003
+    z = synth.normal_f64(5, "acc.logits", (B, k, V)).astype(np.float32)
+    z[0, 2, [5, 900, 4000]] = 7.5                     # exact three-way tie -> lowest index
+    z[1, 0, :] = -1.0
+    z[1, 0, 3], z[1, 0, 1] = 0.0, -0.0                # -0.0 == +0.0: first index wins
+    a = O.argmax_first(z)
+    drafts = synth.uniform_int(5, "acc.drafts", (B, k - 1), 0, V - 1)
+    for b in range(B):                                 # sequence b accepts exactly min(b, k-1) drafts
+        L = min(b, k - 1)
+        drafts[b, :L] = a[b, :L]
+        if L < k - 1:
+            drafts[b, L] = (a[b, L] + 1) % V
+    out = R.accept_from_logits(torch.from_numpy(z).cuda(), torch.from_numpy(drafts).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(out["argmax"].cpu().numpy(), a)
+    assert a[0, 2] == 5 and a[1, 0] == 1
+    for b in range(B):
+        L, committed, bonus = O.accept(drafts[b], a[b])
+        assert int(out["accept_len"][b]) == L == min(b, k - 1)
+        assert out["committed"][b].cpu().tolist() == committed + [-1] * (k - len(committed))
+        assert int(out["next_anchor"][b]) == bonus
+
+
+# ----------------------------------------------------------------------------- tiny workload (real prefix)
+@pytest.fixture(scope="module")
+def tiny(R):
+    wl = WORKLOADS["tiny"]
+    shape, seed = wl.shape, wl.seed
+    src = LazyWeights(shape, seed)
+    prefix = synth_tokens(shape, seed, "tiny.prefix", (1, wl.prefix_len))
+    block = synth_tokens(shape, seed, "tiny.block", (1, 8))
+    w = O.OracleWeights(shape, src, np.float32)
+    okv = O.OracleKV(shape, 1, 256, np.float32)
+    O.prefill(w, okv, prefix)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, 1, 256)
+    ws16 = R.Workspace(model, 1, 16, 256)
+    pt = torch.from_numpy(prefix).cuda()
+    for c0 in range(0, wl.prefix_len, 16):               # causal prefill = verify passes, every row committed
+        R.block_forward(model, cache, ws16, pt[:, c0:c0 + 16].contiguous(), R.VERIFY, want_logits=False)
+        cache.lengths += 16
+    torch.cuda.synchronize()
+    return dict(shape=shape, src=src, w=w, okv=okv, model=model, cache=cache, prefix=prefix, block=block)
+
+
+def test_tiny_prefill_cache(R, tiny):
+    """The GPU's own prefill writes K/V rows within tolerance of the oracle's cache."""
+    t = tiny
+    for l in range(t["shape"].n_layers):
+        kg, vg = t["cache"].read_kv(l, 0, 128)
+        assert rel_err(O.bf16_bits_to_float(kg), t["okv"].k[l][:, :, :128]) < TOL
+        assert rel_err(O.bf16_bits_to_float(vg), t["okv"].v[l][:, :, :128]) < TOL
+
+
+@pytest.mark.parametrize("mode,bidir_from", [(O.VERIFY, 0), (O.DRAFT, 0), (O.DRAFT, 1), (O.DRAFT, 5)])
+def test_tiny_block_pass(R, tiny, mode, bidir_from):
+    t = tiny
+    ref, _, _ = O.block_forward(t["w"], t["okv"], t["block"], mode, bidir_from)
+    ws = R.Workspace(t["model"], 1, 8, 256)
+    logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(t["block"]).cuda(),
+                                 R.VERIFY if mode == O.VERIFY else R.DRAFT, bidir_from)
+    g = logits.cpu().numpy()
+    e = rel_err(g, ref)
+    log("tiny %s bidir_from=%d: rel err %.3e" % (mode, bidir_from, e))
+    assert e <= TOL
+    near = check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+    log("  near-tie argmax rows differing: %s" % near)
+    assert int(t["cache"].lengths.cpu()[0]) == 128
+
+
+def test_tiny_self_speculation_loop(R, tiny):
+    """Three paper-loop steps (draft -> verify -> accept -> commit) on both sides from the same prefix."""
+    t = tiny
+    shape = t["shape"]
+    okv = t["okv"].copy()
+    k = 8
+    anchor = synth_tokens(shape, 0, "tiny.anchor", (1,))
+    model = t["model"]
+    cache = R.DeviceCache(shape, 1, 256)
+    cache.k.copy_(t["cache"].k)
+    cache.v.copy_(t["cache"].v)
+    cache.lengths.copy_(t["cache"].lengths)
+    ws = R.Workspace(model, 1, k, 256)
+    a_o, a_g = anchor.copy(), torch.from_numpy(anchor).cuda()
+    for step in range(3):
+        ref = O.self_spec_step(t["w"], okv, a_o, k)
+        d, dl = R.draft(model, cache, ws, a_g, k, want_logits=True)
+        e_d = rel_err(dl.cpu().numpy(), ref["draft_logits"])
+        assert e_d <= TOL
+        assert np.array_equal(d.cpu().numpy(), ref["drafts"]), "drafts differ (step %d)" % step
+        out = R.verify_accept(model, cache, ws, a_g, d, k, want_logits=True)
+        e_v = rel_err(out["logits"].cpu().numpy(), ref["verify_logits"])
+        assert e_v <= TOL
+        L = int(out["accept_len"].cpu()[0])
+        assert L == int(ref["L"][0])
+        assert out["committed"][0].cpu().tolist()[:L + 1] == ref["committed"][0]
+        assert int(cache.lengths.cpu()[0]) == int(okv.lengths[0])
+        a_o, a_g = ref["next_anchor"], out["next_anchor"]
+        assert int(a_g.cpu()[0]) == int(a_o[0])
+        log("tiny step %d: L=%d draft err %.2e verify err %.2e" % (step, L, e_d, e_v))
+    assert R.read_device_status(ws) == 0
+
+
+def test_tiny_planted_drafts_full_accept(R, tiny):
+    """Drafts equal to the oracle's greedy AR continuation are accepted in full (L = k-1) and the
+    committed rows advance the cache by k."""
+    t = tiny
+    k = 8
+    okv = t["okv"].copy()
+    anchor = synth_tokens(t["shape"], 0, "tiny.anchor", (1,))
+    tok, greedy = anchor.copy(), []
+    for _ in range(k):
+        tok, _ = O.ar_step(t["w"], okv, tok)
+        greedy.append(int(tok[0]))
+    drafts = np.array([greedy[:k - 1]], dtype=np.int32)
+    cache = R.DeviceCache(t["shape"], 1, 256)
+    cache.k.copy_(t["cache"].k)
+    cache.v.copy_(t["cache"].v)
+    cache.lengths.copy_(t["cache"].lengths)
+    ws = R.Workspace(t["model"], 1, k, 256)
+    out = R.verify_accept(t["model"], cache, ws, torch.from_numpy(anchor).cuda(), torch.from_numpy(drafts).cuda(),
+                          k)
+    assert int(out["accept_len"].cpu()[0]) == k - 1
+    assert out["committed"][0].cpu().tolist() == greedy
+    assert int(cache.lengths.cpu()[0]) == 128 + k
+    kg, _ = cache.read_kv(0, 0, 128 + k)
+    assert rel_err(O.bf16_bits_to_float(kg), okv.k[0][:, :, :128 + k]) < TOL
+
+
+def test_capacity_error_is_reported_not_written(R, tiny):
+    """A block that would run past max_len sets the capacity bit; no row beyond the cache is written."""
+    t = tiny
+    cache = R.DeviceCache(t["shape"], 1, 128)
+    cache.set_lengths([124])
+    ws = R.Workspace(t["model"], 1, 8, 128)
+    R.block_forward(t["model"], cache, ws, torch.from_numpy(t["block"]).cuda(), R.VERIFY, want_logits=False)
+    assert R.read_device_status(ws) & 0x2
+    assert R.read_device_status(ws) == 0        # reading clears the sticky bits
+
+
+def test_bad_token_is_reported(R, tiny):
+    t = tiny
+    bad = t["block"].copy()
+    bad[0, 3] = 5000
+    ws = R.Workspace(t["model"], 1, 8, 256)
+    R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(bad).cuda(), R.VERIFY, want_logits=False)
+    assert R.read_device_status(ws) & 0x1
+
+
+# ----------------------------------------------------------------------------- one 8B-shaped layer + LM head
+@pytest.fixture(scope="module")
+def layer8b(R):
+    wl = WORKLOADS["8b_layer"]
+    shape, seed, P = wl.shape, wl.seed, wl.prefix_len
+    src = LazyWeights(shape, seed)
+    kb, vb = prefix_kv(shape, seed, 0, 1, P)
+    w = O.OracleWeights(shape, src, np.float32)
+    okv = O.OracleKV(shape, 1, P + 64, np.float32)
+    okv.set_prefix_bf16(0, kb, vb, [P])
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, 1, P + 64)
+    cache.load_prefix(0, kb, vb)
+    cache.set_lengths([P])
+    return dict(shape=shape, w=w, okv=okv, model=model, cache=cache, seed=seed)
+
+
+@pytest.mark.parametrize("k", [8, 16, 32])
+@pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
+def test_8b_layer_block_pass(R, layer8b, k, mode):
+    t = layer8b
+    shape = t["shape"]
+    tok = synth_tokens(shape, t["seed"], "8b_layer.block%d" % k, (1, k))
+    ref, nk, nv = O.block_forward(t["w"], t["okv"], tok, mode)
+    ws = R.Workspace(t["model"], 1, k, t["cache"].max_len)
+    logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(tok).cuda(),
+                                 R.VERIFY if mode == O.VERIFY else R.DRAFT)
+    g = logits.cpu().numpy()
+    e = rel_err(g, ref)
+    log("8b_layer k=%d %s: rel err %.3e" % (k, mode, e))
+    assert e <= TOL
+    check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+    kg, vg = t["cache"].read_kv(0, 2048, 2048 + k)
+    assert rel_err(O.bf16_bits_to_float(kg), nk[0]) < TOL
+    assert rel_err(O.bf16_bits_to_float(vg), nv[0]) < TOL
+    assert R.read_device_status(ws) == 0
