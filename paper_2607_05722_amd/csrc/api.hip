@@ -75,25 +75,25 @@ int env_int(const char* name, int dflt) {
 
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
-    int M, Mpad, units, n_splits, chunk, attn_waves, rows_pad, lm_tiles, h_tiles, groups;
-    size_t status, ctr_resid0, ctr_resid1, ctr_attn, ctr_fin, ctr_end;
-    size_t x, xg, inv_a, inv_f, part_ss, q, o, act, keys, amax, po, pml, total;
+    int M, Mpad, units, n_splits, chunk, row_tiles, attn_waves, attn_z, rows_pad, lm_tiles, lm_parts;
+    size_t status, x, xg, inv, q, o, act, keys, po, pml, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     Layout L{};
     L.M = batch * k;
     L.Mpad = cdiv(L.M, 64) * 64;
-    L.groups = L.Mpad / 16;
     L.units = batch * c.n_kv_heads;
     const int G = c.n_q_heads / c.n_kv_heads;
-    L.attn_waves = cdiv(G * k, 16);
-    L.rows_pad = L.attn_waves * 16;
+    L.row_tiles = cdiv(G * k, 16);
+    L.attn_z = cdiv(L.row_tiles, 8);
+    L.attn_waves = L.row_tiles < 8 ? (L.row_tiles < 4 ? 4 : L.row_tiles) : 8;
+    L.rows_pad = L.attn_z * 8 * 16;
     L.lm_tiles = cdiv(c.vocab, 16);
-    L.h_tiles = c.hidden / 16;
+    L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
     // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
     const int target = env_int("NLD_ATTN_TARGET_WG", 256);
-    int ns = cdiv(target, L.units);
+    int ns = cdiv(target, L.units * L.attn_z);
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
     if (ns < 1) ns = 1;
@@ -106,25 +106,17 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
         off = align256(off + bytes);
         return o;
     };
-    L.status = take(4);
-    L.ctr_resid0 = take(4 * (size_t)L.groups);
-    L.ctr_resid1 = take(4 * (size_t)L.groups);
-    L.ctr_attn = take(4 * (size_t)L.units);
-    L.ctr_fin = take(4 * (size_t)batch);
-    L.ctr_end = off;
     const size_t H = c.hidden, QD = (size_t)c.n_q_heads * c.head_dim;
+    L.status = take(4);
     L.x = take(4 * L.Mpad * H);
     L.xg = take(2 * L.Mpad * H);
-    L.inv_a = take(4 * (size_t)L.Mpad);
-    L.inv_f = take(4 * (size_t)L.Mpad);
-    L.part_ss = take(4 * L.Mpad * (size_t)L.h_tiles);
+    L.inv = take(4 * (size_t)L.Mpad);
     L.q = take(2 * L.Mpad * QD);
     L.o = take(2 * L.Mpad * QD);
     L.act = take(2 * L.Mpad * (size_t)c.ffn);
-    L.keys = take(8 * L.Mpad * (size_t)L.lm_tiles);
-    L.amax = take(4 * (size_t)L.Mpad);
-    L.po = take(4 * (size_t)L.units * L.n_splits * L.rows_pad * c.head_dim);
-    L.pml = take(4 * 2 * (size_t)L.units * L.n_splits * L.rows_pad);
+    L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
+    L.po = L.n_splits > 1 ? take(4 * (size_t)L.units * L.n_splits * L.rows_pad * c.head_dim) : 0;
+    L.pml = L.n_splits > 1 ? take(4 * 2 * (size_t)L.units * L.n_splits * L.rows_pad) : 0;
     L.total = off;
     return L;
 }
@@ -146,13 +138,34 @@ nld_status check_config(const nld_config* c) {
     return NLD_OK;
 }
 
-// ---------------------------------------------------------------- GEMM launch plan
-struct GemmPlan {
+// ---------------------------------------------------------------- GEMM launch plans
+// Normed multi-tile GEMM: k-steps per wavefront and wavefront count with ks * waves == ksteps.
+bool plan_norm(int M, int ksteps, int* ks, int* waves) {
+    if (M > 16 || env_int("NLD_NO_NORM_GEMM", 0)) return false;
+    const int cand[] = {16, 20, 8, 4};
+    for (int c : cand) {
+        if (ksteps % c == 0 && ksteps / c >= 1 && ksteps / c <= 8 && gemm_norm_supported(c)) {
+            *ks = c;
+            *waves = ksteps / c;
+            return true;
+        }
+    }
+    return false;
+}
+
+// Workgroups for n_tiles tiles: about one per CU, balanced contiguous ranges.
+int norm_grid(int n_tiles) {
+    const int cus = env_int("NLD_CUS", 256);
+    const int per = cdiv(n_tiles, cus);
+    return cdiv(n_tiles, per);
+}
+
+struct StreamPlan {
     int mt, ct, nw, gx, gy;
 };
 
-GemmPlan plan_gemm(int epi, int M, int n_tiles) {
-    GemmPlan p;
+StreamPlan plan_stream(int epi, int M, int n_tiles) {
+    StreamPlan p;
     p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
     p.gy = cdiv(M, 16 * p.mt);
     if (epi == EPI_LMHEAD) {
@@ -167,11 +180,6 @@ GemmPlan plan_gemm(int epi, int M, int n_tiles) {
     }
     p.gx = cdiv(n_tiles, p.ct);
     return p;
-}
-
-hipError_t gemm(int epi, const GemmArgs& a, hipStream_t s) {
-    const GemmPlan p = plan_gemm(epi, a.M, a.n_tiles);
-    return launch_gemm(epi, p.mt, p.ct, p.nw, p.gx, p.gy, a, s);
 }
 
 enum Source { SRC_TOKENS = 0, SRC_DRAFT = 1, SRC_VERIFY = 2 };
@@ -210,6 +218,35 @@ nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, 
     return NLD_OK;
 }
 
+// One projection whose operand is RMSNorm(x) (QKV, gate/up, LM head): the fused
+// normed kernel for M <= 16, else the prep kernel + the streamed kernel.
+hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream_t s, int* parts_out) {
+    int ks = 0, waves = 0;
+    if (plan_norm(g.M, g.ksteps, &ks, &waves)) {
+        const int grid = norm_grid(g.n_tiles);
+        if (parts_out) *parts_out = grid;
+        g.n_parts = grid;
+        return launch_gemm_norm(epi, ks, waves, grid, g, s);
+    }
+    PrepArgs pa{};
+    pa.x = g.x_in;
+    pa.gain = g.gain;
+    pa.eps = g.eps;
+    pa.M = g.M;
+    pa.hidden = g.K;
+    pa.xg = at<uint16_t>(ws, L.xg);
+    pa.inv_rms = at<float>(ws, L.inv);
+    hipError_t e = launch_prep(pa, s);
+    if (e != hipSuccess) return e;
+    g.A = pa.xg;
+    g.lda = g.K;
+    g.inv_rms = pa.inv_rms;
+    const StreamPlan p = plan_stream(epi, g.M, g.n_tiles);
+    if (parts_out) *parts_out = p.gx;
+    g.n_parts = p.gx;
+    return launch_gemm_stream(epi, p.mt, p.ct, p.nw, p.gx, p.gy, g, s);
+}
+
 nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int k, const PassIO& io, void* ws,
                     const Layout& L, hipStream_t s) {
     const nld_config& c = mdl->cfg;
@@ -218,9 +255,6 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     const size_t kv_layer = (size_t)batch * nkv * kv->max_len * D;
     uint32_t* status = at<uint32_t>(ws, L.status);
     float* x = at<float>(ws, L.x);
-    uint16_t* xg = at<uint16_t>(ws, L.xg);
-    float* inv_a = at<float>(ws, L.inv_a);
-    float* inv_f = at<float>(ws, L.inv_f);
 
     EmbedArgs e{};
     e.tokens = io.tokens;
@@ -233,11 +267,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.vocab = c.vocab;
     e.hidden = c.hidden;
     e.embed = (const uint16_t*)mdl->w.embed;
-    e.gain = (const uint16_t*)mdl->layers[0].attn_norm;
-    e.eps = c.rms_eps;
     e.x = x;
-    e.xg = xg;
-    e.inv_rms = inv_a;
     e.status = status;
     {
         TraceScope ts(NLD_TRACE_EMBED, s);
@@ -251,14 +281,14 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         uint16_t* vc = (uint16_t*)kv->v + (size_t)l * kv_layer;
 
         GemmArgs g{};
-        g.A = xg;
-        g.lda = c.hidden;
+        g.x_in = x;
+        g.gain = (const uint16_t*)W.attn_norm;
+        g.eps = c.rms_eps;
         g.M = M;
         g.K = c.hidden;
         g.W = (const uint4*)W.w_qkv;
         g.n_tiles = (nq + 2 * nkv) * D / 16;
         g.ksteps = ks_h;
-        g.inv_rms = inv_a;
         g.q_out = at<uint16_t>(ws, L.q);
         g.kc = kc;
         g.vc = vc;
@@ -272,7 +302,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.status = status;
         {
             TraceScope ts(NLD_TRACE_QKV, s);
-            HIP_TRY(gemm(EPI_QKV, g, s));
+            HIP_TRY(normed_gemm(EPI_QKV, g, ws, L, s, nullptr));
         }
 
         AttnArgs at_{};
@@ -281,9 +311,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.vc = vc;
         at_.lengths = kv->lengths;
         at_.o = at<uint16_t>(ws, L.o);
-        at_.part_o = at<float>(ws, L.po);
-        at_.part_ml = at<float>(ws, L.pml);
-        at_.counters = at<uint32_t>(ws, L.ctr_attn);
+        at_.part_o = L.n_splits > 1 ? at<float>(ws, L.po) : nullptr;
+        at_.part_ml = L.n_splits > 1 ? at<float>(ws, L.pml) : nullptr;
         at_.k_blk = k;
         at_.n_q_heads = nq;
         at_.n_kv_heads = nkv;
@@ -293,10 +322,12 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.mode = io.mode;
         at_.bidir_from = io.bidir_from;
         at_.rows_pad = L.rows_pad;
+        at_.row_tiles = L.row_tiles;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);
-            HIP_TRY(launch_attention(D, L.attn_waves, L.units, at_, s));
+            HIP_TRY(launch_attention(D, L.attn_waves, L.attn_z, L.units, at_, s));
+            if (L.n_splits > 1) HIP_TRY(launch_attention_combine(D, L.units, (nq / nkv) * k, at_, s));
         }
 
         GemmArgs go{};
@@ -305,34 +336,29 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         go.M = M;
         go.K = nq * D;
         go.W = (const uint4*)W.w_o;
-        go.n_tiles = L.h_tiles;
+        go.n_tiles = c.hidden / 16;
         go.ksteps = ks_q;
         go.x = x;
-        go.xg = xg;
-        go.gain = (const uint16_t*)W.ffn_norm;
-        go.part_ss = at<float>(ws, L.part_ss);
-        go.inv_rms_out = inv_f;
-        go.counters = at<uint32_t>(ws, L.ctr_resid0);
-        go.eps = c.rms_eps;
         {
             TraceScope ts(NLD_TRACE_O_PROJ, s);
-            HIP_TRY(gemm(EPI_RESID, go, s));
+            const StreamPlan p = plan_stream(EPI_RESID, M, go.n_tiles);
+            HIP_TRY(launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, go, s));
         }
 
         GemmArgs gu{};
-        gu.A = xg;
-        gu.lda = c.hidden;
+        gu.x_in = x;
+        gu.gain = (const uint16_t*)W.ffn_norm;
+        gu.eps = c.rms_eps;
         gu.M = M;
         gu.K = c.hidden;
         gu.W = (const uint4*)W.w_gate_up;
         gu.n_tiles = cdiv(c.ffn, 8);
         gu.ksteps = ks_h;
-        gu.inv_rms = inv_f;
         gu.act = at<uint16_t>(ws, L.act);
         gu.ffn = c.ffn;
         {
             TraceScope ts(NLD_TRACE_GATE_UP, s);
-            HIP_TRY(gemm(EPI_SWIGLU, gu, s));
+            HIP_TRY(normed_gemm(EPI_SWIGLU, gu, ws, L, s, nullptr));
         }
 
         GemmArgs gd{};
@@ -341,58 +367,51 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gd.M = M;
         gd.K = c.ffn;
         gd.W = (const uint4*)W.w_down;
-        gd.n_tiles = L.h_tiles;
+        gd.n_tiles = c.hidden / 16;
         gd.ksteps = ks_f;
         gd.x = x;
-        gd.xg = xg;
-        gd.gain = (const uint16_t*)(l + 1 < c.n_layers ? mdl->layers[l + 1].attn_norm : mdl->w.final_norm);
-        gd.part_ss = at<float>(ws, L.part_ss);
-        gd.inv_rms_out = inv_a;
-        gd.counters = at<uint32_t>(ws, L.ctr_resid1);
-        gd.eps = c.rms_eps;
         {
             TraceScope ts(NLD_TRACE_DOWN, s);
-            HIP_TRY(gemm(EPI_RESID, gd, s));
+            const StreamPlan p = plan_stream(EPI_RESID, M, gd.n_tiles);
+            HIP_TRY(launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, gd, s));
         }
     }
 
     GemmArgs gl{};
-    gl.A = xg;
-    gl.lda = c.hidden;
+    gl.x_in = x;
+    gl.gain = (const uint16_t*)mdl->w.final_norm;
+    gl.eps = c.rms_eps;
     gl.M = M;
     gl.K = c.hidden;
     gl.W = (const uint4*)mdl->w.lm_head;
     gl.n_tiles = L.lm_tiles;
     gl.ksteps = ks_h;
-    gl.inv_rms = inv_a;
     gl.logits = io.logits;
     gl.part_keys = at<unsigned long long>(ws, L.keys);
     gl.vocab = c.vocab;
+    int parts = 0;
     {
         TraceScope ts(NLD_TRACE_LM_HEAD, s);
-        HIP_TRY(gemm(EPI_LMHEAD, gl, s));
+        HIP_TRY(normed_gemm(EPI_LMHEAD, gl, ws, L, s, &parts));
     }
 
-    ArgmaxArgs am{};
-    am.part_keys = at<unsigned long long>(ws, L.keys);
-    am.n_tiles = L.lm_tiles;
-    am.vocab = c.vocab;
-    am.M = M;
-    am.k_blk = k;
-    am.batch = batch;
-    am.argmax_ws = at<int32_t>(ws, L.amax);
-    am.argmax_out = io.argmax_out;
-    am.finish = io.finish;
-    am.draft_in = io.draft_in;
-    am.draft_out = io.draft_out;
-    am.accept_len = io.accept_len;
-    am.committed = io.committed;
-    am.next_anchor = io.next_anchor;
-    am.lengths = io.advance_lengths ? kv->lengths : nullptr;
-    am.counters = at<uint32_t>(ws, L.ctr_fin);
+    FinishArgs fa{};
+    fa.part_keys = at<unsigned long long>(ws, L.keys);
+    fa.n_parts = parts;
+    fa.vocab = c.vocab;
+    fa.k_blk = k;
+    fa.batch = batch;
+    fa.argmax_out = io.argmax_out;
+    fa.finish = io.finish;
+    fa.draft_in = io.draft_in;
+    fa.draft_out = io.draft_out;
+    fa.accept_len = io.accept_len;
+    fa.committed = io.committed;
+    fa.next_anchor = io.next_anchor;
+    fa.lengths = io.advance_lengths ? kv->lengths : nullptr;
     {
         TraceScope ts(NLD_TRACE_ARGMAX, s);
-        HIP_TRY(launch_argmax_finish(am, s));
+        HIP_TRY(launch_finish(fa, s));
     }
     return NLD_OK;
 }
@@ -585,7 +604,7 @@ nld_status nld_verify_accept(const nld_model* m, const nld_kv_cache* kv, const i
 
 size_t nld_accept_workspace_bytes(int32_t batch, int32_t k) {
     if (batch < 1 || k < 1) return 0;
-    return align256(4) + align256(4 * (size_t)batch) + align256(4 * (size_t)batch * k);
+    return 256;
 }
 
 nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int32_t batch, int32_t k,
@@ -596,22 +615,19 @@ nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int
     if (batch < 1 || k < 1 || k > 64 || vocab < 1) return fail(NLD_ERR_INVALID_ARG, "bad batch, k or vocab");
     if (k > 1 && !draft) return fail(NLD_ERR_INVALID_ARG, "draft is NULL");
     if (ws_bytes < nld_accept_workspace_bytes(batch, k)) return fail(NLD_ERR_CAPACITY, "workspace too small");
-    ArgmaxArgs am{};
-    am.part_keys = nullptr;
-    am.logits = logits;
-    am.vocab = vocab;
-    am.M = batch * k;
-    am.k_blk = k;
-    am.batch = batch;
-    am.counters = (uint32_t*)((char*)workspace + align256(4));
-    am.argmax_ws = (int32_t*)((char*)workspace + align256(4) + align256(4 * (size_t)batch));
-    am.argmax_out = argmax;
-    am.finish = FINISH_ACCEPT;
-    am.draft_in = draft;
-    am.accept_len = accept_len;
-    am.committed = committed;
-    am.next_anchor = next_anchor;
-    HIP_TRY(launch_argmax_finish(am, (hipStream_t)stream));
+    FinishArgs fa{};
+    fa.part_keys = nullptr;
+    fa.logits = logits;
+    fa.vocab = vocab;
+    fa.k_blk = k;
+    fa.batch = batch;
+    fa.argmax_out = argmax;
+    fa.finish = FINISH_ACCEPT;
+    fa.draft_in = draft;
+    fa.accept_len = accept_len;
+    fa.committed = committed;
+    fa.next_anchor = next_anchor;
+    HIP_TRY(launch_finish(fa, (hipStream_t)stream));
     return NLD_OK;
 }
 

@@ -45,23 +45,22 @@ __device__ __forceinline__ int32_t argmax_key_index(unsigned long long key) {
 enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
-    // operands
-    const uint16_t* A;   // bf16 activations [M][lda], row-major
+    // A operand.  Streamed GEMM: bf16 activations A [M][lda].  Normed GEMM:
+    // the fp32 residual stream x_in [M][K] and the RMSNorm gain; the kernel
+    // forms A = bf16(x * gain) and the per-row scale 1/rms(x) itself.
+    const uint16_t* A;
     int lda;
+    const float* x_in;
+    const uint16_t* gain;
+    float eps;
     int M;               // rows
-    int K;               // logical reduction length (multiple of 8)
+    int K;               // reduction length (multiple of 8)
     const uint4* W;      // packed weights: [n_tiles][ksteps][64 lanes] x 16 bytes
     int n_tiles;
     int ksteps;          // ceil(K / 32)
-    const float* inv_rms;  // per-row RMSNorm scale applied to the product (QKV, SWIGLU, LMHEAD)
-    // EPI_RESID: x += A W^T; xg = bf16(x * gain); row sums of squares -> inv_rms_out
+    const float* inv_rms;  // streamed GEMM with a normed operand: per-row scale [M]
+    // EPI_RESID: x += A W^T
     float* x;
-    uint16_t* xg;
-    const uint16_t* gain;
-    float* part_ss;      // [Mpad][n_tiles]
-    float* inv_rms_out;  // [Mpad]
-    uint32_t* counters;  // one per row group (blockIdx.y)
-    float eps;
     // EPI_QKV
     uint16_t* q_out;     // bf16 [M][n_q_heads * head_dim]
     uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
@@ -75,8 +74,9 @@ struct GemmArgs {
     uint16_t* act;       // bf16 [M][ffn]
     int ffn;
     // EPI_LMHEAD
-    float* logits;       // optional f32 [M][vocab]
-    unsigned long long* part_keys;  // [Mpad][n_tiles]
+    float* logits;                   // optional f32 [M][vocab]
+    unsigned long long* part_keys;   // [M][n_parts]: one argmax key per row per workgroup
+    int n_parts;
     int vocab;
 };
 
@@ -88,8 +88,8 @@ struct AttnArgs {
     uint16_t* o;         // bf16 [M][n_q_heads * D]
     float* part_o;       // [units][n_splits][rows_pad][D]
     float* part_ml;      // [units][n_splits][rows_pad][2]
-    uint32_t* counters;  // [units]
     int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
+    int row_tiles;       // query-row tiles of 16 per unit (GQA group size x k / 16, rounded up)
     float scale_log2;    // log2(e) / sqrt(D)
 };
 
@@ -100,23 +100,27 @@ struct EmbedArgs {
     int source;             // 0 tokens, 1 draft block, 2 verify block
     int k_blk, M, mask_id, vocab, hidden;
     const uint16_t* embed;
+    float* x;
+    uint32_t* status;
+};
+
+struct PrepArgs {           // RMSNorm operand for the streamed GEMM path
+    const float* x;
     const uint16_t* gain;
     float eps;
-    float* x;
+    int M, hidden;
     uint16_t* xg;
     float* inv_rms;
-    uint32_t* status;
 };
 
 enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2 };
 
-struct ArgmaxArgs {
-    const unsigned long long* part_keys;  // [Mpad][n_tiles] (or NULL when reducing logits)
-    int n_tiles;
-    const float* logits;                  // [M][vocab] (used when part_keys is NULL)
+struct FinishArgs {
+    const unsigned long long* part_keys;  // [M][n_parts] (or NULL: reduce `logits`)
+    int n_parts;
+    const float* logits;                  // [M][vocab]
     int vocab;
-    int M, k_blk, batch;
-    int32_t* argmax_ws;                   // [M]
+    int k_blk, batch;
     int32_t* argmax_out;                  // optional [M]
     int finish;
     const int32_t* draft_in;              // FINISH_ACCEPT: [batch][k-1]
@@ -125,7 +129,6 @@ struct ArgmaxArgs {
     int32_t* committed;                   // [batch][k]
     int32_t* next_anchor;
     int32_t* lengths;                     // advanced by L+1 (may be NULL)
-    uint32_t* counters;                   // [batch]
 };
 
 enum PackKind { PACK_LINEAR = 0, PACK_QKV = 1, PACK_GATE_UP = 2 };
@@ -144,8 +147,15 @@ struct PackArgs {
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
-hipError_t launch_gemm(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a, hipStream_t s);
-hipError_t launch_attention(int head_dim, int waves, int units, const AttnArgs& a, hipStream_t s);
-hipError_t launch_argmax_finish(const ArgmaxArgs& a, hipStream_t s);
+hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
+// Normed multi-tile GEMM (M <= 16).  ks = k-steps per wavefront (ksteps = ks * waves); grid = workgroups.
+bool gemm_norm_supported(int ks);
+hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs& a, hipStream_t s);
+// Streamed GEMM: 16*mt rows x 16*ct columns per workgroup, nw wavefronts split K.
+hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
+                              hipStream_t s);
+hipError_t launch_attention(int head_dim, int waves, int zslices, int units, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);
+hipError_t launch_finish(const FinishArgs& a, hipStream_t s);
 
 }  // namespace nld
