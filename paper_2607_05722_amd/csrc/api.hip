@@ -76,7 +76,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_waves, attn_z, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, inv, q, o, act, keys, po, pml, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, po, pml, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -87,7 +87,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     const int G = c.n_q_heads / c.n_kv_heads;
     L.row_tiles = cdiv(G * k, 16);
     L.attn_z = cdiv(L.row_tiles, 8);
-    L.attn_waves = L.row_tiles < 8 ? (L.row_tiles < 4 ? 4 : L.row_tiles) : 8;
+    L.attn_waves = L.row_tiles <= 4 ? 4 : 8;   // 256 or 512 threads share each stage's loads
     L.rows_pad = L.attn_z * 8 * 16;
     L.lm_tiles = cdiv(c.vocab, 16);
     L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
@@ -96,6 +96,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     int ns = cdiv(target, L.units * L.attn_z);
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
+    if (ns > 256) ns = 256;
     if (ns < 1) ns = 1;
     L.chunk = cdiv(cdiv(max_len, ns), 64) * 64;
     L.n_splits = cdiv(max_len, L.chunk);
@@ -110,10 +111,10 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.status = take(4);
     L.x = take(4 * L.Mpad * H);
     L.xg = take(2 * L.Mpad * H);
-    L.inv = take(4 * (size_t)L.Mpad);
+    L.part_ss = take(4 * L.Mpad * (H / 16));
     L.q = take(2 * L.Mpad * QD);
     L.o = take(2 * L.Mpad * QD);
-    L.act = take(2 * L.Mpad * (size_t)c.ffn);
+    L.act = take(2 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
     L.po = L.n_splits > 1 ? take(4 * (size_t)L.units * L.n_splits * L.rows_pad * c.head_dim) : 0;
     L.pml = L.n_splits > 1 ? take(4 * 2 * (size_t)L.units * L.n_splits * L.rows_pad) : 0;
@@ -140,11 +141,14 @@ nld_status check_config(const nld_config* c) {
 
 // ---------------------------------------------------------------- GEMM launch plans
 // Normed multi-tile GEMM: k-steps per wavefront and wavefront count with ks * waves == ksteps.
-bool plan_norm(int M, int ksteps, int* ks, int* waves) {
+bool plan_norm(int epi, int M, int ksteps, int* ks, int* waves) {
     if (M > 16 || env_int("NLD_NO_NORM_GEMM", 0)) return false;
-    const int cand[] = {16, 20, 8, 4};
+    // k-steps per wavefront: 16 (8 wavefronts) where the epilogue needs registers, 8 (16 wavefronts) for SwiGLU
+    const int pref = env_int(epi == EPI_QKV ? "NLD_NORM_KS_QKV" : epi == EPI_SWIGLU ? "NLD_NORM_KS_GU" : "NLD_NORM_KS_LM",
+                             epi == EPI_SWIGLU ? 8 : 16);
+    const int cand[] = {pref, 8, 16, 20, 4};
     for (int c : cand) {
-        if (ksteps % c == 0 && ksteps / c >= 1 && ksteps / c <= 8 && gemm_norm_supported(c)) {
+        if (gemm_norm_supported(c) && ksteps % c == 0 && ksteps / c >= 1 && ksteps / c <= gemm_norm_max_waves(c)) {
             *ks = c;
             *waves = ksteps / c;
             return true;
@@ -218,29 +222,20 @@ nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, 
     return NLD_OK;
 }
 
-// One projection whose operand is RMSNorm(x) (QKV, gate/up, LM head): the fused
-// normed kernel for M <= 16, else the prep kernel + the streamed kernel.
+// One projection whose operand is RMSNorm(x) (QKV, gate/up, LM head): the normed
+// multi-tile kernel for M <= 16, else the streamed kernel (both read the bf16
+// operand and the row statistics the producer of x wrote).
 hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream_t s, int* parts_out) {
+    g.A = at<uint16_t>(ws, L.xg);
+    g.part_ss = at<float>(ws, L.part_ss);
+    g.n_ss = g.K / 16;
     int ks = 0, waves = 0;
-    if (plan_norm(g.M, g.ksteps, &ks, &waves)) {
+    if (plan_norm(epi, g.M, g.ksteps, &ks, &waves)) {
         const int grid = norm_grid(g.n_tiles);
         if (parts_out) *parts_out = grid;
         g.n_parts = grid;
         return launch_gemm_norm(epi, ks, waves, grid, g, s);
     }
-    PrepArgs pa{};
-    pa.x = g.x_in;
-    pa.gain = g.gain;
-    pa.eps = g.eps;
-    pa.M = g.M;
-    pa.hidden = g.K;
-    pa.xg = at<uint16_t>(ws, L.xg);
-    pa.inv_rms = at<float>(ws, L.inv);
-    hipError_t e = launch_prep(pa, s);
-    if (e != hipSuccess) return e;
-    g.A = pa.xg;
-    g.lda = g.K;
-    g.inv_rms = pa.inv_rms;
     const StreamPlan p = plan_stream(epi, g.M, g.n_tiles);
     if (parts_out) *parts_out = p.gx;
     g.n_parts = p.gx;
@@ -267,7 +262,10 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.vocab = c.vocab;
     e.hidden = c.hidden;
     e.embed = (const uint16_t*)mdl->w.embed;
+    e.gain = (const uint16_t*)mdl->layers[0].attn_norm;
     e.x = x;
+    e.xg = at<uint16_t>(ws, L.xg);
+    e.part_ss = at<float>(ws, L.part_ss);
     e.status = status;
     {
         TraceScope ts(NLD_TRACE_EMBED, s);
@@ -281,8 +279,6 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         uint16_t* vc = (uint16_t*)kv->v + (size_t)l * kv_layer;
 
         GemmArgs g{};
-        g.x_in = x;
-        g.gain = (const uint16_t*)W.attn_norm;
         g.eps = c.rms_eps;
         g.M = M;
         g.K = c.hidden;
@@ -298,7 +294,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.n_kv_heads = nkv;
         g.head_dim = D;
         g.max_len = kv->max_len;
-        g.log2_base = log2((double)c.rope_base);
+        for (int i = 0; i < D / 2; ++i) g.inv_freq[i] = pow((double)c.rope_base, -2.0 * i / (double)D);
         g.status = status;
         {
             TraceScope ts(NLD_TRACE_QKV, s);
@@ -332,13 +328,15 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
 
         GemmArgs go{};
         go.A = at<uint16_t>(ws, L.o);
-        go.lda = nq * D;
         go.M = M;
         go.K = nq * D;
         go.W = (const uint4*)W.w_o;
         go.n_tiles = c.hidden / 16;
         go.ksteps = ks_q;
         go.x = x;
+        go.xg_out = at<uint16_t>(ws, L.xg);
+        go.gain_next = (const uint16_t*)W.ffn_norm;
+        go.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_O_PROJ, s);
             const StreamPlan p = plan_stream(EPI_RESID, M, go.n_tiles);
@@ -346,8 +344,6 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         }
 
         GemmArgs gu{};
-        gu.x_in = x;
-        gu.gain = (const uint16_t*)W.ffn_norm;
         gu.eps = c.rms_eps;
         gu.M = M;
         gu.K = c.hidden;
@@ -363,13 +359,15 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
 
         GemmArgs gd{};
         gd.A = at<uint16_t>(ws, L.act);
-        gd.lda = c.ffn;
         gd.M = M;
         gd.K = c.ffn;
         gd.W = (const uint4*)W.w_down;
         gd.n_tiles = c.hidden / 16;
         gd.ksteps = ks_f;
         gd.x = x;
+        gd.xg_out = at<uint16_t>(ws, L.xg);
+        gd.gain_next = (const uint16_t*)(l + 1 < c.n_layers ? mdl->layers[l + 1].attn_norm : mdl->w.final_norm);
+        gd.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_DOWN, s);
             const StreamPlan p = plan_stream(EPI_RESID, M, gd.n_tiles);
@@ -378,8 +376,6 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     }
 
     GemmArgs gl{};
-    gl.x_in = x;
-    gl.gain = (const uint16_t*)mdl->w.final_norm;
     gl.eps = c.rms_eps;
     gl.M = M;
     gl.K = c.hidden;

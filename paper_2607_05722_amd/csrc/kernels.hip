@@ -49,8 +49,10 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsig
 // GEMM epilogues.  v holds C[4g+i][r] of a 16x16 output tile (rows mbase..+16, packed
 // column tile t); lane = 16g + r.  inv(i) is the RMSNorm scale of row mbase+4g+i.
 // =====================================================================================
-template <typename InvFn>
-__device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, InvFn inv) {
+// pos(i): absolute position of row mbase+4g+i (block row j at P_b + j).
+template <typename InvFn, typename PosFn>
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, InvFn inv,
+                                        PosFn pos_of) {
     const int r = lane & 15, g = lane >> 4;
     const int D = a.head_dim;
     const int tiles_per_head = D / 16;
@@ -59,26 +61,26 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
     const int dim = (r < 8) ? fi : D / 2 + fi;  // lanes r and r^8 hold the pair (fi, fi + D/2)
     const int nq = a.n_q_heads, nkv = a.n_kv_heads;
     const int kind = hh < nq ? 0 : (hh < nq + nkv ? 1 : 2);
-    const double inv_freq = exp2(-(2.0 * (double)fi / (double)D) * a.log2_base);
+    const double inv_freq = a.inv_freq[fi];
     const double two_pi = 6.283185307179586476925286766559;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int m = mbase + 4 * g + i;
         const bool ok = m < a.M;
-        const int mm = ok ? m : 0;
         const float y = v[i] * inv(i);
         const float partner = __shfl_xor(y, 8);
-        const int b = mm / a.k_blk, j = mm % a.k_blk;
-        const int pos = committed_length(a.lengths, b, a.max_len, a.status) + j;
+        const int pos = pos_of(i);
         float out = y;
         if (kind < 2) {
+            // angle pos * base^(-2 fi / D) reduced to [-pi, pi] in fp64, then sin/cos in fp32
             double ang = (double)pos * inv_freq;
-            ang -= two_pi * rint(ang / two_pi);
-            float sn, cs;
-            sincosf((float)ang, &sn, &cs);
+            ang -= two_pi * rint(ang * (1.0 / two_pi));
+            const float af = (float)ang;
+            const float sn = __sinf(af), cs = __cosf(af);
             out = (r < 8) ? (y * cs - partner * sn) : (y * cs + partner * sn);
         }
         if (!ok) continue;
+        const int b = m / a.k_blk;
         const uint16_t ob = (uint16_t)f32_to_bf16(out);
         if (kind == 0) {
             a.q_out[(size_t)m * (nq * D) + hh * D + dim] = ob;
@@ -106,7 +108,7 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, f32x4_t v, int mba
         if (m < a.M && r < 8 && col < a.ffn) {
             const float gate = y, up = partner;
             const float act = gate / (1.0f + expf(-gate)) * up;
-            a.act[(size_t)m * a.ffn + col] = (uint16_t)f32_to_bf16(act);
+            a.act[opnd_index(m, col, (a.ffn + 31) / 32)] = (uint16_t)f32_to_bf16(act);
         }
     }
 }
@@ -131,14 +133,45 @@ __device__ __forceinline__ void epi_lmhead(const GemmArgs& a, f32x4_t v, int mba
     }
 }
 
-__device__ __forceinline__ void epi_resid(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane) {
+// xres[i]: the residual x[mbase+4g+i][16t+r], loaded when the workgroup started.
+// Writes x += v, the next RMSNorm's bf16 operand x * gain_next and, per row, the
+// sum of x^2 over the tile's 16 columns.
+__device__ __forceinline__ void epi_resid(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, const float (&xres)[4]) {
     const int r = lane & 15, g = lane >> 4;
     const int N = a.n_tiles * 16;
     const int n = t * 16 + r;
+    const float gn = bf16_to_f32(a.gain_next[n]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int m = mbase + 4 * g + i;
-        if (m < a.M) a.x[(size_t)m * N + n] += v[i];
+        const bool ok = m < a.M;
+        const float xn = xres[i] + v[i];
+        if (ok) {
+            a.x[(size_t)m * N + n] = xn;
+            a.xg_out[opnd_index(m, n, N / 32)] = (uint16_t)f32_to_bf16(xn * gn);
+        }
+        float sq = ok ? xn * xn : 0.f;
+        sq += __shfl_xor(sq, 1);
+        sq += __shfl_xor(sq, 2);
+        sq += __shfl_xor(sq, 4);
+        sq += __shfl_xor(sq, 8);
+        if (r == 0 && ok) a.part_ss_out[(size_t)m * a.n_tiles + t] = sq;
+    }
+}
+
+// 1/rms for `rows` rows starting at m0 from the producer's 16-column partial sums
+// (fixed summation order); rows past M get 0.  One wavefront per row.
+__device__ __forceinline__ void rms_scales(const GemmArgs& a, int m0, int rows, float* inv_s) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    for (int rr = wave; rr < rows; rr += nw) {
+        const int m = m0 + rr;
+        float s = 0.f;
+        if (m < a.M) {
+            const float* ps = a.part_ss + (size_t)m * a.n_ss;
+            for (int p = lane; p < a.n_ss; p += 64) s += ps[p];
+        }
+        s = wave_sum(s);
+        if (lane == 0) inv_s[rr] = (m < a.M) ? 1.0f / sqrtf(s / (float)a.K + a.eps) : 0.f;
     }
 }
 
@@ -153,11 +186,11 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, f32x4_t v, int mbas
 // products meet in LDS and one wavefront (rotating) runs the epilogue.
 // =====================================================================================
 template <int KS, int EPI>
-__global__ void __launch_bounds__(512) gemm_norm_kernel(GemmArgs a) {
+__global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmArgs a) {
     __shared__ f32x4_t red[2][16][64];
-    __shared__ float ss_part[16][16];
     __shared__ float inv_s[16];
     __shared__ unsigned long long key_s[16][16];
+    __shared__ int pos_s[16];
 
     const int NW = blockDim.x >> 6;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -167,70 +200,61 @@ __global__ void __launch_bounds__(512) gemm_norm_kernel(GemmArgs a) {
     const int te = (int)((long long)T * (blockIdx.x + 1) / G);
     const int s0 = wave * KS;
 
-    constexpr int KH = KS / 2;   // weights stream in half-tiles: one half-tile in flight ahead
-    auto load_w = [&](int t, int half, uint4 (&buf)[KH]) {
-        const uint4* p = a.W + ((size_t)t * a.ksteps + s0 + half * KH) * 64 + lane;
+    // Weight tiles stream through two register buffers: the first two tiles are
+    // requested before the operand prologue, and tile t+2 as soon as tile t's
+    // MFMAs have read their registers, so two tiles are in flight throughout.
+    auto load_w = [&](int t, uint4 (&buf)[KS]) {
+        const uint4* p = a.W + ((size_t)t * a.ksteps + s0) * 64 + lane;
 #pragma unroll
-        for (int s = 0; s < KH; ++s) buf[s] = p[(size_t)s * 64];
+        for (int s = 0; s < KS; ++s) buf[s] = p[(size_t)s * 64];
     };
-    uint4 wb0[KH], wb1[KH];
-    if (tb < te) load_w(tb, 0, wb0);
+    uint4 wb0[KS], wb1[KS];
+    if (tb < te) load_w(tb, wb0);
+    if (tb + 1 < te) load_w(tb + 1, wb1);
 
-    // operand slice: row r, columns 32*(s0+s) + 8g .. +8
+    // operand slice: row r, columns 32*(s0+s) + 8g .. +8 of bf16(x * gain)
     uint4 areg[KS];
-    float ss = 0.f;
     const bool row_ok = r < a.M;
-    const float* xr = a.x_in + (size_t)(row_ok ? r : 0) * a.K;
+    const uint16_t* ar = a.A + ((size_t)s0 * 64 + lane) * 8;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-        const int col = 32 * (s0 + s) + 8 * g;
-        uint4 packed = {0u, 0u, 0u, 0u};
-        if (row_ok) {
-            const float4 x0 = *(const float4*)(xr + col);
-            const float4 x1 = *(const float4*)(xr + col + 4);
-            const uint4 gg = *(const uint4*)(a.gain + col);
-            ss += x0.x * x0.x + x0.y * x0.y + x0.z * x0.z + x0.w * x0.w;
-            ss += x1.x * x1.x + x1.y * x1.y + x1.z * x1.z + x1.w * x1.w;
-            packed.x = f32_to_bf16(x0.x * bf16_to_f32(gg.x & 0xFFFFu)) | (f32_to_bf16(x0.y * bf16_to_f32(gg.x >> 16)) << 16);
-            packed.y = f32_to_bf16(x0.z * bf16_to_f32(gg.y & 0xFFFFu)) | (f32_to_bf16(x0.w * bf16_to_f32(gg.y >> 16)) << 16);
-            packed.z = f32_to_bf16(x1.x * bf16_to_f32(gg.z & 0xFFFFu)) | (f32_to_bf16(x1.y * bf16_to_f32(gg.z >> 16)) << 16);
-            packed.w = f32_to_bf16(x1.z * bf16_to_f32(gg.w & 0xFFFFu)) | (f32_to_bf16(x1.w * bf16_to_f32(gg.w >> 16)) << 16);
+    for (int s = 0; s < KS; ++s) areg[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 512) : uint4{0u, 0u, 0u, 0u};
+    rms_scales(a, 0, 16, inv_s);
+    if constexpr (EPI == EPI_QKV) {
+        if (threadIdx.x < 16) {   // absolute position of block row m: P_b + j
+            const int m = min((int)threadIdx.x, a.M - 1);
+            pos_s[threadIdx.x] = committed_length(a.lengths, m / a.k_blk, a.max_len, a.status) + m % a.k_blk;
         }
-        areg[s] = packed;
-    }
-    ss += __shfl_xor(ss, 16);
-    ss += __shfl_xor(ss, 32);
-    if (g == 0) ss_part[wave][r] = ss;
-    __syncthreads();
-    if (threadIdx.x < 16) {
-        float tot = 0.f;
-        for (int w = 0; w < NW; ++w) tot += ss_part[w][threadIdx.x];
-        inv_s[threadIdx.x] = ((int)threadIdx.x < a.M) ? 1.0f / sqrtf(tot / (float)a.K + a.eps) : 0.f;
     }
     __syncthreads();
     auto inv = [&](int i) { return inv_s[4 * g + i]; };
+    auto pos_of = [&](int i) { return pos_s[4 * g + i]; };
 
     unsigned long long key_run[4] = {0ull, 0ull, 0ull, 0ull};
     auto finish_tile = [&](int t, int parity) {
         f32x4_t v = red[parity][0][lane];
         for (int w = 1; w < NW; ++w) v += red[parity][w][lane];
-        if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv);
+        if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv, pos_of);
         else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, 0, t, lane, inv);
         else epi_lmhead(a, v, 0, t, lane, inv, key_run);
     };
 
-    for (int t = tb; t < te; ++t) {
-        load_w(t, 1, wb1);
+    for (int t = tb; t < te; t += 2) {
         f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < KH; ++s) acc = mfma_16x16x32(areg[s], wb0[s], acc);
-        if (t + 1 < te) load_w(t + 1, 0, wb0);
-#pragma unroll
-        for (int s = 0; s < KH; ++s) acc = mfma_16x16x32(areg[KH + s], wb1[s], acc);
-        const int parity = (t - tb) & 1;
-        red[parity][wave][lane] = acc;
+        for (int s = 0; s < KS; ++s) acc = mfma_16x16x32(areg[s], wb0[s], acc);
+        if (t + 2 < te) load_w(t + 2, wb0);
+        red[0][wave][lane] = acc;
         __syncthreads();
-        if (wave == (t - tb) % NW) finish_tile(t, parity);
+        if (wave == (t - tb) % NW) finish_tile(t, 0);
+        if (t + 1 < te) {
+            acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < KS; ++s) acc = mfma_16x16x32(areg[s], wb1[s], acc);
+            if (t + 3 < te) load_w(t + 3, wb1);
+            red[1][wave][lane] = acc;
+            __syncthreads();
+            if (wave == (t + 1 - tb) % NW) finish_tile(t + 1, 1);
+        }
     }
 
     if constexpr (EPI == EPI_LMHEAD) {
@@ -248,7 +272,7 @@ __global__ void __launch_bounds__(512) gemm_norm_kernel(GemmArgs a) {
     }
 }
 
-bool gemm_norm_supported(int ks) { return ks == 4 || ks == 8 || ks == 16 || ks == 20; }  // even: half-tiles
+bool gemm_norm_supported(int ks) { return ks == 4 || ks == 8 || ks == 16 || ks == 20; }
 
 template <int KS>
 static hipError_t launch_norm_ks(int epi, int waves, int grid, const GemmArgs& a, hipStream_t s) {
@@ -262,8 +286,10 @@ static hipError_t launch_norm_ks(int epi, int waves, int grid, const GemmArgs& a
     return hipGetLastError();
 }
 
+int gemm_norm_max_waves(int ks) { return ks >= 16 ? 8 : 16; }
+
 hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs& a, hipStream_t s) {
-    if (waves < 1 || waves > 8) return hipErrorInvalidValue;
+    if (waves < 1 || waves > gemm_norm_max_waves(ks)) return hipErrorInvalidValue;
     switch (ks) {
         case 4: return launch_norm_ks<4>(epi, waves, grid, a, s);
         case 8: return launch_norm_ks<8>(epi, waves, grid, a, s);
@@ -278,7 +304,7 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // workgroup; the NW wavefronts split the reduction, each streaming its slice of the
 // weights and of the bf16 activations with one batch in flight ahead of the MFMAs.
 // Used for the O and down projections (residual epilogue) and, for M > 16, for
-// every projection (the RMSNorm operand then comes from rmsnorm_prep_kernel).
+// every projection (the per-row RMSNorm scale is then formed in the prologue).
 // =====================================================================================
 template <int MT, int CT>
 struct Batch {
@@ -293,6 +319,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     constexpr int U = B::U;
     __shared__ f32x4_t red[NW][MT * CT][64];
     __shared__ unsigned long long key_s[16 * MT];
+    __shared__ float inv_s[16 * MT];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -314,9 +341,8 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     bool aok[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        const int m = m0 + mt * 16 + r;
-        aok[mt] = m < a.M;
-        ap[mt] = a.A + (size_t)(aok[mt] ? m : 0) * a.lda + 8 * g;
+        aok[mt] = m0 + mt * 16 + r < a.M;
+        ap[mt] = a.A + ((size_t)(blockIdx.y * MT + mt) * a.ksteps * 64 + lane) * 8;
     }
 
     f32x4_t acc[MT][CT];
@@ -324,6 +350,20 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // residual values for the epilogue of this wavefront's first tile, fetched up front
+    float xres[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (EPI == EPI_RESID) {
+        if (wave < MT * CT) {
+            const int mt = wave / CT, ct = wave % CT;
+            const int n = (t0 + ct) * 16 + r;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = m0 + 16 * mt + 4 * g + i;
+                if (m < a.M && t0 + ct < a.n_tiles) xres[i] = a.x[(size_t)m * a.n_tiles * 16 + n];
+            }
+        }
+    }
 
     const uint4 zero4 = {0u, 0u, 0u, 0u};
     auto load = [&](int s, B& buf) {
@@ -336,7 +376,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
             const int kcol = ss * 32 + 8 * g;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                buf.x[u][mt] = (in && aok[mt] && kcol < a.K) ? *(const uint4*)(ap[mt] + (size_t)ss * 32) : zero4;
+                buf.x[u][mt] = (in && aok[mt] && kcol < a.K) ? *(const uint4*)(ap[mt] + (size_t)ss * 512) : zero4;
         }
     };
     auto compute = [&](const B& buf) {
@@ -350,6 +390,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
 
     B b0, b1;
     load(s_begin, b0);
+    if constexpr (EPI != EPI_RESID) rms_scales(a, m0, 16 * MT, inv_s);   // visible after the barrier below
     for (int s = s_begin; s < s_end; s += 2 * U) {
         load(s + U, b1);
         compute(b0);
@@ -373,12 +414,22 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         const int t = t0 + ct;
         if (t >= a.n_tiles) continue;
         const int mbase = m0 + 16 * mt;
-        auto inv = [&](int i) {
-            const int m = mbase + 4 * g + i;
-            return m < a.M ? a.inv_rms[m] : 0.f;
+        auto inv = [&](int i) { return inv_s[16 * mt + 4 * g + i]; };
+        auto pos_of = [&](int i) {
+            const int m = min(mbase + 4 * g + i, a.M - 1);
+            return committed_length(a.lengths, m / a.k_blk, a.max_len, a.status) + m % a.k_blk;
         };
-        if constexpr (EPI == EPI_RESID) epi_resid(a, v, mbase, t, lane);
-        else if constexpr (EPI == EPI_QKV) epi_qkv(a, v, mbase, t, lane, inv);
+        if constexpr (EPI == EPI_RESID) {
+            if (ti != wave) {   // only when a wavefront finishes more than one tile
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int m = mbase + 4 * g + i;
+                    xres[i] = m < a.M ? a.x[(size_t)m * a.n_tiles * 16 + t * 16 + r] : 0.f;
+                }
+            }
+            epi_resid(a, v, mbase, t, lane, xres);
+        }
+        else if constexpr (EPI == EPI_QKV) epi_qkv(a, v, mbase, t, lane, inv, pos_of);
         else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, mbase, t, lane, inv);
         else {
             unsigned long long kr[4] = {0ull, 0ull, 0ull, 0ull};
@@ -430,28 +481,6 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
     }
 }
 
-// RMSNorm operand for the streamed path: xg = bf16(x * gain), inv_rms = 1/rms(x).
-__global__ void __launch_bounds__(256) rmsnorm_prep_kernel(PrepArgs a) {
-    __shared__ float red[4];
-    const int m = blockIdx.x;
-    const float* x = a.x + (size_t)m * a.hidden;
-    float ss = 0.f;
-    for (int c = threadIdx.x; c < a.hidden; c += blockDim.x) {
-        const float v = x[c];
-        ss += v * v;
-        a.xg[(size_t)m * a.hidden + c] = (uint16_t)f32_to_bf16(v * bf16_to_f32(a.gain[c]));
-    }
-    ss = wave_sum(ss);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-    __syncthreads();
-    if (threadIdx.x == 0) a.inv_rms[m] = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)a.hidden + a.eps);
-}
-
-hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
-    rmsnorm_prep_kernel<<<a.M, 256, 0, s>>>(a);
-    return hipGetLastError();
-}
-
 // =====================================================================================
 // Block-masked GQA attention.  Workgroup = (key split, sequence x KV head, row slice);
 // one compute wavefront per 16 query rows of the GQA group (rows = heads of the
@@ -494,8 +523,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     __shared__ uint4 lds_k[2][C::KCHUNKS];
     __shared__ uint4 lds_v[2][C::VCHUNKS];
 
-    const int nthreads = blockDim.x;
-    const int cpt = C::CHUNKS / nthreads;
+    const int nthreads = blockDim.x;   // 256 or 512: the stage loops below cover any count >= 256
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, unit = blockIdx.y;
@@ -527,8 +555,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     auto gload = [&](int kb) {
 #pragma unroll
         for (int i = 0; i < CPT_MAX; ++i) {
-            if (i >= cpt) break;
             const int q = threadIdx.x + i * nthreads;
+            if (q >= C::CHUNKS) break;
             if (q < C::KCHUNKS) {
                 stg[i] = *(const uint4*)(kbase + (size_t)kb * D + (size_t)q * 8);
             } else {
@@ -550,8 +578,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     auto lstore = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < CPT_MAX; ++i) {
-            if (i >= cpt) break;
             const int q = threadIdx.x + i * nthreads;
+            if (q >= C::CHUNKS) break;
             if (q < C::KCHUNKS) {
                 const int kr = q / C::KCH, c = q % C::KCH;
                 lds_k[buf][kr * C::KCH + (c ^ kswz<D>(kr))] = stg[i];
@@ -656,11 +684,11 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     if (a.n_splits == 1) {
         if (row_ok) {
             const float inv = 1.0f / l_tot;
-            uint16_t* op = a.o + (size_t)m * HD + head * D;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) op[16 * dt + 4 * g + i] = (uint16_t)f32_to_bf16(acc[dt][i] * inv);
+                for (int i = 0; i < 4; ++i)
+                    a.o[opnd_index(m, head * D + 16 * dt + 4 * g + i, HD / 32)] = (uint16_t)f32_to_bf16(acc[dt][i] * inv);
         }
         return;
     }
@@ -674,42 +702,64 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
 // Merge of the key splits: one workgroup per (unit, query row), one thread per head dim.
 template <int D>
 __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
+    __shared__ float wsh[256];
+    __shared__ float inv_den;
     const int unit = blockIdx.x, rw = blockIdx.y, d = threadIdx.x;
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv, k = a.k_blk;
-    const size_t ubase = (size_t)unit * a.n_splits * a.rows_pad + rw;
-    float mx = -INFINITY;
-    for (int sp = 0; sp < a.n_splits; ++sp) mx = fmaxf(mx, a.part_ml[(ubase + (size_t)sp * a.rows_pad) * 2]);
-    float num = 0.f, den = 0.f;
+    const int ns = a.n_splits;
+    const size_t ubase = (size_t)unit * ns * a.rows_pad + rw;
+    // split statistics -> weights exp2(m_s - max) in LDS (ns <= 256)
+    float ms = -INFINITY, ls = 0.f;
+    for (int sp = d; sp < ns; sp += D) {
+        const float2 ml = *(const float2*)(a.part_ml + (ubase + (size_t)sp * a.rows_pad) * 2);
+        wsh[sp] = ml.x;
+        ms = fmaxf(ms, ml.x);
+    }
+    // block max over D threads (D <= 128: two wavefronts at most)
+    ms = fmaxf(ms, __shfl_xor(ms, 32));
+    ms = fmaxf(ms, __shfl_xor(ms, 16));
+    ms = fmaxf(ms, __shfl_xor(ms, 8));
+    ms = fmaxf(ms, __shfl_xor(ms, 4));
+    ms = fmaxf(ms, __shfl_xor(ms, 2));
+    ms = fmaxf(ms, __shfl_xor(ms, 1));
+    __shared__ float wmax[2];
+    if ((d & 63) == 0) wmax[d >> 6] = ms;
+    __syncthreads();
+    const float mx = (D > 64) ? fmaxf(wmax[0], wmax[1]) : wmax[0];
+    for (int sp = d; sp < ns; sp += D) {
+        const float msp = wsh[sp];
+        const float w = (msp == -INFINITY) ? 0.f : exp2f(msp - mx);
+        ls += w * a.part_ml[(ubase + (size_t)sp * a.rows_pad) * 2 + 1];
+        wsh[sp] = w;
+    }
+    ls += __shfl_xor(ls, 32);
+    ls += __shfl_xor(ls, 16);
+    ls += __shfl_xor(ls, 8);
+    ls += __shfl_xor(ls, 4);
+    ls += __shfl_xor(ls, 2);
+    ls += __shfl_xor(ls, 1);
+    __shared__ float wden[2];
+    if ((d & 63) == 0) wden[d >> 6] = ls;
+    __syncthreads();
+    if (d == 0) inv_den = 1.0f / ((D > 64) ? (wden[0] + wden[1]) : wden[0]);
+    __syncthreads();
+    float num = 0.f;
     int sp = 0;
-    for (; sp + 4 <= a.n_splits; sp += 4) {
-        float ms[4], ls[4], os[4];
+    for (; sp + 8 <= ns; sp += 8) {
+        float os[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const size_t pb = ubase + (size_t)(sp + e) * a.rows_pad;
-            ms[e] = a.part_ml[pb * 2];
-            ls[e] = a.part_ml[pb * 2 + 1];
-            os[e] = a.part_o[pb * D + d];
-        }
+        for (int e = 0; e < 8; ++e) os[e] = a.part_o[(ubase + (size_t)(sp + e) * a.rows_pad) * D + d];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float w = (ms[e] == -INFINITY) ? 0.f : exp2f(ms[e] - mx);
-            num += w * os[e];
-            den += w * ls[e];
-        }
+        for (int e = 0; e < 8; ++e) num += wsh[sp + e] * os[e];
     }
-    for (; sp < a.n_splits; ++sp) {
-        const size_t pb = ubase + (size_t)sp * a.rows_pad;
-        const float ms = a.part_ml[pb * 2];
-        const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
-        num += w * a.part_o[pb * D + d];
-        den += w * a.part_ml[pb * 2 + 1];
-    }
+    for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)sp * a.rows_pad) * D + d];
     const int hl = rw / k, j = rw % k;
-    a.o[(size_t)(b * k + j) * a.n_q_heads * D + (kvh * G + hl) * D + d] = (uint16_t)f32_to_bf16(num / den);
+    a.o[opnd_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32)] = (uint16_t)f32_to_bf16(num * inv_den);
 }
 
 hipError_t launch_attention(int head_dim, int waves, int zslices, int units, const AttnArgs& a, hipStream_t s) {
+    if (waves != 4 && waves != 8) return hipErrorInvalidValue;
     const dim3 grid(a.n_splits, units, zslices);
     if (head_dim == 128) attention_kernel<128><<<grid, waves * 64, 0, s>>>(a);
     else if (head_dim == 64) attention_kernel<64><<<grid, waves * 64, 0, s>>>(a);
@@ -741,7 +791,33 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
         tok = 0;
     }
     const uint16_t* e = a.embed + (size_t)tok * a.hidden;
-    for (int c = threadIdx.x; c < a.hidden; c += blockDim.x) a.x[(size_t)m * a.hidden + c] = bf16_to_f32(e[c]);
+    const size_t row = (size_t)m * a.hidden;
+    const int chunks = a.hidden / 16;
+    for (int c = threadIdx.x; c < chunks; c += blockDim.x) {   // 16 columns per thread
+        float ss = 0.f;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int col = 16 * c + 8 * h;
+            const uint4 w = *(const uint4*)(e + col);
+            const uint4 gg = *(const uint4*)(a.gain + col);
+            const uint32_t ew[4] = {w.x, w.y, w.z, w.w}, gw[4] = {gg.x, gg.y, gg.z, gg.w};
+            float xv[8];
+            uint32_t xb[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                xv[2 * q] = bf16_to_f32(ew[q] & 0xFFFFu);
+                xv[2 * q + 1] = bf16_to_f32(ew[q] >> 16);
+                xb[q] = f32_to_bf16(xv[2 * q] * bf16_to_f32(gw[q] & 0xFFFFu)) |
+                        (f32_to_bf16(xv[2 * q + 1] * bf16_to_f32(gw[q] >> 16)) << 16);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ss += xv[q] * xv[q];
+            *(float4*)(a.x + row + col) = float4{xv[0], xv[1], xv[2], xv[3]};
+            *(float4*)(a.x + row + col + 4) = float4{xv[4], xv[5], xv[6], xv[7]};
+            *(uint4*)(a.xg + opnd_index(m, col, a.hidden / 32)) = uint4{xb[0], xb[1], xb[2], xb[3]};
+        }
+        a.part_ss[(size_t)m * chunks + c] = ss;
+    }
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {

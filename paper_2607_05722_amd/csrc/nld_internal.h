@@ -41,26 +41,37 @@ __device__ __forceinline__ int32_t argmax_key_index(unsigned long long key) {
     return (int32_t)(0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull));
 }
 
+// Activation operands (the A side of every projection) are stored in MFMA
+// operand order: rows in tiles of 16, columns in steps of 32; tile mt, step s
+// is one 1 KiB block whose 16-byte lane l holds A[16mt + l%16][32s + 8(l/16) .. +8],
+// so a wavefront fetches one operand with one contiguous 1 KiB load.
+__host__ __device__ __forceinline__ size_t opnd_index(int m, int k, int ksteps) {
+    return ((size_t)((m >> 4) * ksteps + (k >> 5)) * 64 + (size_t)((((k & 31) >> 3) << 4) + (m & 15))) * 8 + (k & 7);
+}
+
 // ---------------------------------------------------------------- kernel arguments
 enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
-    // A operand.  Streamed GEMM: bf16 activations A [M][lda].  Normed GEMM:
-    // the fp32 residual stream x_in [M][K] and the RMSNorm gain; the kernel
-    // forms A = bf16(x * gain) and the per-row scale 1/rms(x) itself.
+    // A operand: bf16 activations in operand order (opnd_index with `ksteps`).
+    // For the projections whose input is RMSNorm(x) (QKV, gate/up, LM head) A is
+    // bf16(x * gain), written by the kernel that produced x, and part_ss holds that
+    // producer's sums of x^2 over 16-column chunks ([M][n_ss]); the consumer turns
+    // them into 1/rms per row.
     const uint16_t* A;
-    int lda;
-    const float* x_in;
-    const uint16_t* gain;
+    const float* part_ss;
+    int n_ss;
     float eps;
     int M;               // rows
     int K;               // reduction length (multiple of 8)
     const uint4* W;      // packed weights: [n_tiles][ksteps][64 lanes] x 16 bytes
     int n_tiles;
     int ksteps;          // ceil(K / 32)
-    const float* inv_rms;  // streamed GEMM with a normed operand: per-row scale [M]
-    // EPI_RESID: x += A W^T
+    // EPI_RESID: x += A W^T, then the next RMSNorm's operand and statistics
     float* x;
+    uint16_t* xg_out;          // bf16(x * gain_next), operand order with N/32 steps
+    const uint16_t* gain_next;
+    float* part_ss_out;        // [M][N/16]
     // EPI_QKV
     uint16_t* q_out;     // bf16 [M][n_q_heads * head_dim]
     uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
@@ -68,10 +79,10 @@ struct GemmArgs {
     const int32_t* lengths;
     int k_blk;
     int n_q_heads, n_kv_heads, head_dim, max_len;
-    double log2_base;
+    double inv_freq[64];  // RoPE frequencies base^(-2i/head_dim), i < head_dim/2 (computed on the host in fp64)
     uint32_t* status;
     // EPI_SWIGLU
-    uint16_t* act;       // bf16 [M][ffn]
+    uint16_t* act;       // bf16 silu(gate) * up, operand order with ceil(ffn/32) steps
     int ffn;
     // EPI_LMHEAD
     float* logits;                   // optional f32 [M][vocab]
@@ -85,7 +96,7 @@ struct AttnArgs {
     const uint16_t* kc;  // this layer's K cache
     const uint16_t* vc;  // this layer's V cache (64-position transposed tiles)
     const int32_t* lengths;
-    uint16_t* o;         // bf16 [M][n_q_heads * D]
+    uint16_t* o;         // bf16 attention output, operand order with n_q_heads*D/32 steps
     float* part_o;       // [units][n_splits][rows_pad][D]
     float* part_ml;      // [units][n_splits][rows_pad][2]
     int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
@@ -100,17 +111,11 @@ struct EmbedArgs {
     int source;             // 0 tokens, 1 draft block, 2 verify block
     int k_blk, M, mask_id, vocab, hidden;
     const uint16_t* embed;
+    const uint16_t* gain;   // first layer's attention RMSNorm gain
     float* x;
+    uint16_t* xg;           // operand order with hidden/32 steps
+    float* part_ss;         // [M][hidden/16]
     uint32_t* status;
-};
-
-struct PrepArgs {           // RMSNorm operand for the streamed GEMM path
-    const float* x;
-    const uint16_t* gain;
-    float eps;
-    int M, hidden;
-    uint16_t* xg;
-    float* inv_rms;
 };
 
 enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2 };
@@ -147,11 +152,12 @@ struct PackArgs {
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
-hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
 // Normed multi-tile GEMM (M <= 16).  ks = k-steps per wavefront (ksteps = ks * waves); grid = workgroups.
 bool gemm_norm_supported(int ks);
+int gemm_norm_max_waves(int ks);
 hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs& a, hipStream_t s);
 // Streamed GEMM: 16*mt rows x 16*ct columns per workgroup, nw wavefronts split K.
+// normed: the operand is an RMSNorm output (per-row scale from part_ss).
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
 hipError_t launch_attention(int head_dim, int waves, int zslices, int units, const AttnArgs& a, hipStream_t s);
