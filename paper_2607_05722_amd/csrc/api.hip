@@ -9,6 +9,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 using namespace nld;
@@ -75,7 +76,7 @@ int env_int(const char* name, int dflt) {
 
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
-    int M, Mpad, units, n_splits, chunk, row_tiles, attn_waves, attn_z, rows_pad, lm_tiles, lm_parts;
+    int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
     size_t status, x, xg, part_ss, q, o, act, keys, po, pml, total;
 };
 
@@ -86,9 +87,9 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.units = batch * c.n_kv_heads;
     const int G = c.n_q_heads / c.n_kv_heads;
     L.row_tiles = cdiv(G * k, 16);
-    L.attn_z = cdiv(L.row_tiles, 8);
-    L.attn_waves = L.row_tiles <= 4 ? 4 : 8;   // 256 or 512 threads share each stage's loads
-    L.rows_pad = L.attn_z * 8 * 16;
+    L.attn_kh = L.row_tiles <= 4 ? 2 : 1;          // wavefronts per row tile (each takes half of a stage's keys)
+    L.attn_z = cdiv(L.row_tiles, 8 / L.attn_kh);
+    L.rows_pad = L.attn_z * (8 / L.attn_kh) * 16;
     L.lm_tiles = cdiv(c.vocab, 16);
     L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
     // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
@@ -96,10 +97,11 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     int ns = cdiv(target, L.units * L.attn_z);
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
-    if (ns > 256) ns = 256;
+    if (ns > 256) ns = 256;   // the merge handles up to 256 partials per row
     if (ns < 1) ns = 1;
     L.chunk = cdiv(cdiv(max_len, ns), 64) * 64;
     L.n_splits = cdiv(max_len, L.chunk);
+    L.n_parts = L.n_splits;   // key halves are merged inside the workgroup
 
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -112,12 +114,12 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.x = take(4 * L.Mpad * H);
     L.xg = take(2 * L.Mpad * H);
     L.part_ss = take(4 * L.Mpad * (H / 16));
-    L.q = take(2 * L.Mpad * QD);
+    L.q = take(2 * std::max(L.Mpad * QD, (size_t)L.units * L.row_tiles * 16 * c.head_dim));
     L.o = take(2 * L.Mpad * QD);
     L.act = take(2 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
-    L.po = L.n_splits > 1 ? take(4 * (size_t)L.units * L.n_splits * L.rows_pad * c.head_dim) : 0;
-    L.pml = L.n_splits > 1 ? take(4 * 2 * (size_t)L.units * L.n_splits * L.rows_pad) : 0;
+    L.po = L.n_parts > 1 ? take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim) : 0;
+    L.pml = L.n_parts > 1 ? take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad) : 0;
     L.total = off;
     return L;
 }
@@ -286,6 +288,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.n_tiles = (nq + 2 * nkv) * D / 16;
         g.ksteps = ks_h;
         g.q_out = at<uint16_t>(ws, L.q);
+        g.q_row_tiles = L.row_tiles;
         g.kc = kc;
         g.vc = vc;
         g.lengths = kv->lengths;
@@ -307,8 +310,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.vc = vc;
         at_.lengths = kv->lengths;
         at_.o = at<uint16_t>(ws, L.o);
-        at_.part_o = L.n_splits > 1 ? at<float>(ws, L.po) : nullptr;
-        at_.part_ml = L.n_splits > 1 ? at<float>(ws, L.pml) : nullptr;
+        at_.part_o = L.n_parts > 1 ? at<float>(ws, L.po) : nullptr;
+        at_.part_ml = L.n_parts > 1 ? at<float>(ws, L.pml) : nullptr;
         at_.k_blk = k;
         at_.n_q_heads = nq;
         at_.n_kv_heads = nkv;
@@ -319,11 +322,12 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.bidir_from = io.bidir_from;
         at_.rows_pad = L.rows_pad;
         at_.row_tiles = L.row_tiles;
+        at_.n_parts = L.n_parts;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);
-            HIP_TRY(launch_attention(D, L.attn_waves, L.attn_z, L.units, at_, s));
-            if (L.n_splits > 1) HIP_TRY(launch_attention_combine(D, L.units, (nq / nkv) * k, at_, s));
+            HIP_TRY(launch_attention(D, L.attn_kh, L.attn_z, L.units, at_, s));
+            if (L.n_parts > 1) HIP_TRY(launch_attention_combine(D, L.units, (nq / nkv) * k, at_, s));
         }
 
         GemmArgs go{};

@@ -83,7 +83,9 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
         const int b = m / a.k_blk;
         const uint16_t ob = (uint16_t)f32_to_bf16(out);
         if (kind == 0) {
-            a.q_out[(size_t)m * (nq * D) + hh * D + dim] = ob;
+            const int G = nq / nkv;
+            const int row = (hh % G) * a.k_blk + (m - b * a.k_blk);
+            a.q_out[q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D)] = ob;
         } else if (pos >= a.max_len) {
             atomicOr(a.status, DEV_CAPACITY);
         } else if (kind == 1) {
@@ -203,7 +205,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     // Weight tiles stream through two register buffers: the first two tiles are
     // requested before the operand prologue, and tile t+2 as soon as tile t's
     // MFMAs have read their registers, so two tiles are in flight throughout.
-    auto load_w = [&](int t, uint4 (&buf)[KS]) {
+    auto load_w = [&](int t, uint4 (&buf)[KS]) __attribute__((always_inline)) {
         const uint4* p = a.W + ((size_t)t * a.ksteps + s0) * 64 + lane;
 #pragma unroll
         for (int s = 0; s < KS; ++s) buf[s] = p[(size_t)s * 64];
@@ -230,7 +232,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     auto pos_of = [&](int i) { return pos_s[4 * g + i]; };
 
     unsigned long long key_run[4] = {0ull, 0ull, 0ull, 0ull};
-    auto finish_tile = [&](int t, int parity) {
+    auto finish_tile = [&](int t, int parity) __attribute__((always_inline)) {
         f32x4_t v = red[parity][0][lane];
         for (int w = 1; w < NW; ++w) v += red[parity][w][lane];
         if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv, pos_of);
@@ -366,7 +368,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     }
 
     const uint4 zero4 = {0u, 0u, 0u, 0u};
-    auto load = [&](int s, B& buf) {
+    auto load = [&](int s, B& buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int ss = s + u;
@@ -379,7 +381,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
                 buf.x[u][mt] = (in && aok[mt] && kcol < a.K) ? *(const uint4*)(ap[mt] + (size_t)ss * 512) : zero4;
         }
     };
-    auto compute = [&](const B& buf) {
+    auto compute = [&](const B& buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -514,30 +516,31 @@ __device__ __forceinline__ int stage_key(int tau, int rho) {
     return 32 * (tau >> 1) + 8 * (rho >> 2) + 4 * (tau & 1) + (rho & 3);
 }
 
-template <int D>
+template <int D, int KH>
 __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     typedef AttnCfg<D> C;
     constexpr int DC = D / 32;
     constexpr int DT = D / 16;
-    constexpr int CPT_MAX = C::CHUNKS / 256;   // chunks per thread with >= 4 wavefronts
-    __shared__ uint4 lds_k[2][C::KCHUNKS];
-    __shared__ uint4 lds_v[2][C::VCHUNKS];
+    constexpr int NT = 512;                    // threads per workgroup
+    constexpr int CPT = C::CHUNKS / NT;        // stage chunks per thread
+    constexpr int RZ = 8 / KH;                 // row tiles per workgroup
+    constexpr int TPW = 4 / KH;                // S tiles (16 keys) per wavefront per stage
+    constexpr float RESCALE_SLACK = 8.0f;      // log2 headroom before the reference max moves
+    // two stage slots, each K tile (KCHUNKS) followed by the V tile (VCHUNKS)
+    __shared__ uint4 lds[2 * C::CHUNKS];
 
-    const int nthreads = blockDim.x;   // 256 or 512: the stage loops below cover any count >= 256
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, unit = blockIdx.y;
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv;
     const int k = a.k_blk, R = G * k;
-    const int HD = a.n_q_heads * D;
-    const int rt = blockIdx.z * 8 + wave;            // this wavefront's row tile
-    const bool computes = wave < 8 && rt < a.row_tiles;
+    const int kh = wave / RZ;                  // which half of each stage's keys (KH == 2)
+    const int rt = blockIdx.z * RZ + (wave % RZ);
+    const bool computes = rt < a.row_tiles;
     const int row = rt * 16 + r;
     const bool row_ok = computes && row < R;
-    const int hl = row_ok ? row / k : 0, j = row_ok ? row % k : 0;
-    const int m = b * k + j;
-    const int head = kvh * G + hl;
+    const int j = row_ok ? row % k : 0;
 
     int P = a.lengths[b];
     P = P < 0 ? 0 : (P > a.max_len ? a.max_len : P);
@@ -550,139 +553,192 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const uint16_t* kbase = a.kc + head_off;
     const uint16_t* vbase = a.vc + head_off;
 
-    // stage loads: chunk q < KCHUNKS is K row q/KCH, chunk q%KCH; otherwise V row (q-KCHUNKS)/8, chunk %8
-    uint4 stg[CPT_MAX];
-    auto gload = [&](int kb) {
+    // per-thread stage chunks: global offsets within a stage and LDS slots (swizzled)
+    int goff[CPT], loff[CPT];
 #pragma unroll
-        for (int i = 0; i < CPT_MAX; ++i) {
-            const int q = threadIdx.x + i * nthreads;
-            if (q >= C::CHUNKS) break;
-            if (q < C::KCHUNKS) {
-                stg[i] = *(const uint4*)(kbase + (size_t)kb * D + (size_t)q * 8);
-            } else {
-                const int qv = q - C::KCHUNKS;
-                stg[i] = *(const uint4*)(vbase + (size_t)(kb >> 6) * D * 64 + (size_t)qv * 8);
-                const int key0 = kb + 8 * (qv & 7);
-                if (key0 + 8 > kend) {      // zero V beyond the valid keys (cache rows there may hold anything)
-                    uint32_t w[4] = {stg[i].x, stg[i].y, stg[i].z, stg[i].w};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const bool lo = key0 + 2 * e < kend, hi = key0 + 2 * e + 1 < kend;
-                        w[e] = (lo ? (w[e] & 0xFFFFu) : 0u) | (hi ? (w[e] & 0xFFFF0000u) : 0u);
-                    }
-                    stg[i] = uint4{w[0], w[1], w[2], w[3]};
-                }
-            }
+    for (int i = 0; i < CPT; ++i) {
+        const int q = threadIdx.x + i * NT;
+        if (q < C::KCHUNKS) {
+            const int kr = q / C::KCH, c = q % C::KCH;
+            goff[i] = q * 8;                                   // relative to kbase + kb * D
+            loff[i] = kr * C::KCH + (c ^ kswz<D>(kr));
+        } else {
+            const int qv = q - C::KCHUNKS, d = qv >> 3, c = qv & 7;
+            goff[i] = qv * 8;                                  // relative to the V tile
+            loff[i] = C::KCHUNKS + d * 8 + (c ^ vswz(d));      // V slots follow the K slots
         }
+    }
+    struct Stage {
+        uint4 v[CPT];
     };
-    auto lstore = [&](int buf) {
+    auto gload = [&](int kb) __attribute__((always_inline)) {
+        Stage st;
+        const uint16_t* kp = kbase + (size_t)kb * D;
+        const uint16_t* vp = vbase + (size_t)(kb >> 6) * D * 64;
 #pragma unroll
-        for (int i = 0; i < CPT_MAX; ++i) {
-            const int q = threadIdx.x + i * nthreads;
-            if (q >= C::CHUNKS) break;
-            if (q < C::KCHUNKS) {
-                const int kr = q / C::KCH, c = q % C::KCH;
-                lds_k[buf][kr * C::KCH + (c ^ kswz<D>(kr))] = stg[i];
-            } else {
-                const int qv = q - C::KCHUNKS;
-                const int d = qv >> 3, c = qv & 7;
-                lds_v[buf][d * 8 + (c ^ vswz(d))] = stg[i];
-            }
+        for (int i = 0; i < CPT; ++i) {
+            const bool is_k = threadIdx.x + i * NT < C::KCHUNKS;   // resolved at compile time for most i
+            st.v[i] = *(const uint4*)((is_k ? kp : vp) + goff[i]);
         }
+        return st;
     };
+    auto lstore = [&](const Stage& st, int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) lds[buf * C::CHUNKS + loff[i]] = st.v[i];
+    };
+
+    // operand offsets in LDS (per lane, fixed for every stage)
+    int koff[TPW][DC], voff[TPW / 2][DT];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+        const int kr = stage_key(TPW * kh + tt, r);
+#pragma unroll
+        for (int c = 0; c < DC; ++c) koff[tt][c] = kr * C::KCH + ((4 * c + g) ^ kswz<D>(kr));
+    }
+#pragma unroll
+    for (int kk = 0; kk < TPW / 2; ++kk) {
+        const int ks = (TPW / 2) * kh + kk;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const int d = 16 * dt + r;
+            voff[kk][dt] = d * 8 + ((4 * ks + g) ^ vswz(d));
+        }
+    }
 
     const uint4 zero4 = {0u, 0u, 0u, 0u};
     uint4 qb[DC];
+    {
+        const uint16_t* qp = a.q + ((size_t)((unit * a.row_tiles + rt) * DC) * 64 + lane) * 8;
 #pragma unroll
-    for (int c = 0; c < DC; ++c)
-        qb[c] = row_ok ? *(const uint4*)(a.q + (size_t)m * HD + head * D + 32 * c + 8 * g) : zero4;
+        for (int c = 0; c < DC; ++c) qb[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 512) : zero4;
+    }
 
     f32x4_t acc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_part = 0.f;
+    // p = exp2(s - m_ref): m_ref only moves when a score exceeds it by RESCALE_SLACK,
+    // so the accumulators are rescaled rarely (any reference gives the same ratio).
+    float m_ref = -INFINITY, l_part = 0.f;
 
-    const int nstages = kend > kbeg ? (kend - kbeg + 63) / 64 : 0;
-    if (nstages > 0) {
-        gload(kbeg);
-        lstore(0);
-    }
-    __syncthreads();
-    for (int st = 0; st < nstages; ++st) {
-        const int kb = kbeg + 64 * st;
-        const int buf = st & 1;
-        if (st + 1 < nstages) gload(kb + 64);
-        if (computes) {
-            f32x4_t s[4];
+    auto compute = [&](int kb, int buf) __attribute__((always_inline)) {
+        if (!computes) return;
+        f32x4_t s[TPW];
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau) {
-                const int kr = stage_key(tau, r);
-                s[tau] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int tt = 0; tt < TPW; ++tt) {
+            s[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int c = 0; c < DC; ++c) {
-                    const uint4 kv4 = lds_k[buf][kr * C::KCH + ((4 * c + g) ^ kswz<D>(kr))];
-                    s[tau] = mfma_16x16x32(kv4, qb[c], s[tau]);
-                }
-            }
-            float sv[16];
-            float mloc = -INFINITY;
+            for (int c = 0; c < DC; ++c) s[tt] = mfma_16x16x32(lds[buf * C::CHUNKS + koff[tt][c]], qb[c], s[tt]);
+        }
+        const bool edge = (kb + 64 > P) || (kb + 64 > kend);   // stage touches the block or the split end
+        float sv[4 * TPW];
+        float mloc = -INFINITY;
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
+        for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = kb + stage_key(tau, 4 * g + i);
+            for (int i = 0; i < 4; ++i) {
+                float x = s[tt][i] * a.scale_log2;
+                if (edge) {
+                    const int key = kb + stage_key(TPW * kh + tt, 4 * g + i);
                     const bool vis = key < kend && (key < P || (key - P) <= j || bidir_row);
-                    const float x = vis ? s[tau][i] * a.scale_log2 : -INFINITY;
-                    sv[tau * 4 + i] = x;
-                    mloc = fmaxf(mloc, x);
+                    x = vis ? x : -INFINITY;
                 }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-            const float m_new = fmaxf(m_run, mloc);
-            float alpha = 1.f;
-            float p[16];
-            if (m_new == -INFINITY) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) p[e] = 0.f;
-            } else {
-                alpha = exp2f(m_run - m_new);
-#pragma unroll
-                for (int e = 0; e < 16; ++e) p[e] = exp2f(sv[e] - m_new);
+                sv[tt * 4 + i] = x;
+                mloc = fmaxf(mloc, x);
             }
-            float psum = 0.f;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) psum += p[e];
-            l_part = l_part * alpha + psum;
-            m_run = m_new;
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        if (mloc > m_ref + RESCALE_SLACK) {        // new reference: rescale what has accumulated
+            const float alpha = __builtin_amdgcn_exp2f(m_ref - mloc);   // 0 when m_ref = -inf
+            l_part *= alpha;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) acc[dt] *= alpha;
+            m_ref = mloc;
+        }
+        float p[4 * TPW];
+        float psum = 0.f;
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                // slot jj of lane group g <-> key kb + 32ks + 8g + jj
-                uint4 pop;
-                const float* pp = p + 8 * ks;
-                pop.x = f32_to_bf16(pp[0]) | (f32_to_bf16(pp[1]) << 16);
-                pop.y = f32_to_bf16(pp[2]) | (f32_to_bf16(pp[3]) << 16);
-                pop.z = f32_to_bf16(pp[4]) | (f32_to_bf16(pp[5]) << 16);
-                pop.w = f32_to_bf16(pp[6]) | (f32_to_bf16(pp[7]) << 16);
+        for (int e = 0; e < 4 * TPW; ++e) {
+            p[e] = __builtin_amdgcn_exp2f(sv[e] - m_ref);   // -inf - finite -> 0; m_ref finite once any key is visible
+            psum += p[e];
+        }
+        if (m_ref == -INFINITY) psum = 0.f;
+        l_part += psum;
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    const int d = 16 * dt + r;
-                    const uint4 vop = lds_v[buf][d * 8 + ((4 * ks + g) ^ vswz(d))];
-                    acc[dt] = mfma_16x16x32(vop, pop, acc[dt]);
+        for (int kk = 0; kk < TPW / 2; ++kk) {
+            const int ks = (TPW / 2) * kh + kk;          // 32-key PV step within the stage
+            // slot jj of lane group g <-> key kb + 32ks + 8g + jj
+            const float* pp = p + 8 * kk;
+            uint4 pop = {pack_bf16x2(pp[0], pp[1]), pack_bf16x2(pp[2], pp[3]), pack_bf16x2(pp[4], pp[5]),
+                         pack_bf16x2(pp[6], pp[7])};
+            if (m_ref == -INFINITY) pop = zero4;
+            const int key0 = kb + 32 * ks + 8 * g;
+            const bool vmask = edge && (key0 + 8 > kend);  // V rows past the valid keys may hold anything
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                uint4 vop = lds[buf * C::CHUNKS + C::KCHUNKS + voff[kk][dt]];
+                if (vmask) {
+                    uint32_t w[4] = {vop.x, vop.y, vop.z, vop.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        w[e] = (key0 + 2 * e < kend ? (w[e] & 0xFFFFu) : 0u) | (key0 + 2 * e + 1 < kend ? (w[e] & 0xFFFF0000u) : 0u);
+                    vop = uint4{w[0], w[1], w[2], w[3]};
                 }
+                acc[dt] = mfma_16x16x32(vop, pop, acc[dt]);
             }
         }
-        if (st + 1 < nstages) lstore(buf ^ 1);
+    };
+
+    // stages of 64 keys; two stages in flight in registers while one is multiplied from LDS
+    const int nst = kend > kbeg ? (kend - kbeg + 63) / 64 : 0;
+    Stage n1{}, n2{};
+    if (nst > 0) {
+        lstore(gload(kbeg), 0);
+        if (nst > 1) n1 = gload(kbeg + 64);
+        if (nst > 2) n2 = gload(kbeg + 128);
+    }
+    __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+        compute(kbeg + 64 * st, st & 1);
+        if (st + 1 < nst) lstore(n1, (st + 1) & 1);
+        n1 = n2;
+        if (st + 3 < nst) n2 = gload(kbeg + 64 * (st + 3));
         __syncthreads();
     }
 
-    if (!computes) return;
     float l_tot = l_part + __shfl_xor(l_part, 16);
     l_tot += __shfl_xor(l_tot, 32);
-
-    if (a.n_splits == 1) {
+    if constexpr (KH == 2) {
+        // merge the two key halves of each row tile through LDS (the stage buffers are free now)
+        float* mrg = (float*)lds;                    // [RZ][16 rows][D + 2] floats, within the 2 stage slots
+        float* slot = mrg + ((size_t)(wave % RZ) * 16 + r) * (D + 2);
+        if (kh == 1 && computes) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) slot[16 * dt + 4 * g + i] = acc[dt][i];
+            if (g == 0) {
+                slot[D] = m_ref;
+                slot[D + 1] = l_tot;
+            }
+        }
+        __syncthreads();
+        if (kh == 1 || !computes) return;
+        const float m2 = slot[D], l2 = slot[D + 1];
+        const float mm = fmaxf(m_ref, m2);
+        const float w1 = (m_ref == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_ref - mm);
+        const float w2 = (m2 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[dt][i] = acc[dt][i] * w1 + slot[16 * dt + 4 * g + i] * w2;
+        l_tot = l_tot * w1 + l2 * w2;
+        m_ref = mm;
+    }
+    if (!computes) return;
+    const int HD = a.n_q_heads * D;
+    if (a.n_parts == 1) {
         if (row_ok) {
+            const int m = b * k + j, head = kvh * G + row / k;
             const float inv = 1.0f / l_tot;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -692,11 +748,11 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         }
         return;
     }
-    const size_t pbase = ((size_t)unit * a.n_splits + split) * a.rows_pad + row;
+    const size_t pbase = ((size_t)unit * a.n_parts + split) * a.rows_pad + row;
     float* po = a.part_o + pbase * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) *(float4*)(po + 16 * dt + 4 * g) = float4{acc[dt][0], acc[dt][1], acc[dt][2], acc[dt][3]};
-    if (g == 0) *(float2*)(a.part_ml + pbase * 2) = float2{m_run, l_tot};
+    if (g == 0) *(float2*)(a.part_ml + pbase * 2) = float2{m_ref, l_tot};
 }
 
 // Merge of the key splits: one workgroup per (unit, query row), one thread per head dim.
@@ -707,7 +763,7 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     const int unit = blockIdx.x, rw = blockIdx.y, d = threadIdx.x;
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv, k = a.k_blk;
-    const int ns = a.n_splits;
+    const int ns = a.n_parts;
     const size_t ubase = (size_t)unit * ns * a.rows_pad + rw;
     // split statistics -> weights exp2(m_s - max) in LDS (ns <= 256)
     float ms = -INFINITY, ls = 0.f;
@@ -758,11 +814,12 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     a.o[opnd_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32)] = (uint16_t)f32_to_bf16(num * inv_den);
 }
 
-hipError_t launch_attention(int head_dim, int waves, int zslices, int units, const AttnArgs& a, hipStream_t s) {
-    if (waves != 4 && waves != 8) return hipErrorInvalidValue;
+hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
     const dim3 grid(a.n_splits, units, zslices);
-    if (head_dim == 128) attention_kernel<128><<<grid, waves * 64, 0, s>>>(a);
-    else if (head_dim == 64) attention_kernel<64><<<grid, waves * 64, 0, s>>>(a);
+    if (head_dim == 128 && kh == 2) attention_kernel<128, 2><<<grid, 512, 0, s>>>(a);
+    else if (head_dim == 128 && kh == 1) attention_kernel<128, 1><<<grid, 512, 0, s>>>(a);
+    else if (head_dim == 64 && kh == 2) attention_kernel<64, 2><<<grid, 512, 0, s>>>(a);
+    else if (head_dim == 64 && kh == 1) attention_kernel<64, 1><<<grid, 512, 0, s>>>(a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

@@ -14,11 +14,15 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 // ---------------------------------------------------------------- numerics helpers
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-// float -> bfloat16, round to nearest even (finite inputs)
+// float -> bfloat16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
+    return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
+}
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+// two floats -> packed bfloat16 pair (lo in bits 0..15), one conversion instruction
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
 // C[16x16] += A[16x32] * B[32x16].  Lane l supplies A[l%16][8(l/16)..+8] and
@@ -73,7 +77,8 @@ struct GemmArgs {
     const uint16_t* gain_next;
     float* part_ss_out;        // [M][N/16]
     // EPI_QKV
-    uint16_t* q_out;     // bf16 [M][n_q_heads * head_dim]
+    uint16_t* q_out;     // bf16 queries in the attention's operand order (q_index)
+    int q_row_tiles;     // query-row tiles of 16 per (sequence, KV head)
     uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
     uint16_t* vc;        // this layer's V cache [batch][n_kv_heads][max_len/64][head_dim][64]
     const int32_t* lengths;
@@ -91,8 +96,15 @@ struct GemmArgs {
     int vocab;
 };
 
+// Queries are stored per (sequence b, KV head) unit with the unit's rows
+// (row = local head * k + block row j) in tiles of 16 and head dims in steps of
+// 32, in MFMA operand order: one 1 KiB block per (row tile, step).
+__host__ __device__ __forceinline__ size_t q_index(int unit, int row, int d, int row_tiles, int D) {
+    return ((size_t)((unit * row_tiles + (row >> 4)) * (D >> 5) + (d >> 5)) * 64 + (size_t)((((d & 31) >> 3) << 4) + (row & 15))) * 8 + (d & 7);
+}
+
 struct AttnArgs {
-    const uint16_t* q;   // bf16 [M][n_q_heads * D]
+    const uint16_t* q;   // bf16 queries (q_index)
     const uint16_t* kc;  // this layer's K cache
     const uint16_t* vc;  // this layer's V cache (64-position transposed tiles)
     const int32_t* lengths;
@@ -101,6 +113,7 @@ struct AttnArgs {
     float* part_ml;      // [units][n_splits][rows_pad][2]
     int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
     int row_tiles;       // query-row tiles of 16 per unit (GQA group size x k / 16, rounded up)
+    int n_parts;         // partial results per (unit, row): n_splits x key halves
     float scale_log2;    // log2(e) / sqrt(D)
 };
 
@@ -160,7 +173,8 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // normed: the operand is an RMSNorm output (per-row scale from part_ss).
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
-hipError_t launch_attention(int head_dim, int waves, int zslices, int units, const AttnArgs& a, hipStream_t s);
+// kh: key halves per stage (2 when the unit has at most 4 row tiles, else 1); 8 wavefronts per workgroup.
+hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s);
 
