@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, po, pml, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, po, pml, blk_k, blk_v, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -94,14 +94,14 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
     // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
     const int target = env_int("NLD_ATTN_TARGET_WG", 256);
-    int ns = cdiv(target, L.units * L.attn_z);
+    int ns = target / (L.units * L.attn_z) - 1;    // one workgroup per (unit, row slice) is the block part
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
-    if (ns > 256) ns = 256;   // the merge handles up to 256 partials per row
+    if (ns > 255) ns = 255;   // the merge handles up to 256 partials per row
     if (ns < 1) ns = 1;
     L.chunk = cdiv(cdiv(max_len, ns), 64) * 64;
     L.n_splits = cdiv(max_len, L.chunk);
-    L.n_parts = L.n_splits;   // key halves are merged inside the workgroup
+    L.n_parts = L.n_splits + 1;   // prefix splits + the block part (key halves merge inside the workgroup)
 
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -112,14 +112,17 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     const size_t H = c.hidden, QD = (size_t)c.n_q_heads * c.head_dim;
     L.status = take(4);
     L.x = take(4 * L.Mpad * H);
-    L.xg = take(2 * L.Mpad * H);
+    L.xg = take(4 * L.Mpad * H);   // split operand (hi and lo bf16)
     L.part_ss = take(4 * L.Mpad * (H / 16));
-    L.q = take(2 * std::max(L.Mpad * QD, (size_t)L.units * L.row_tiles * 16 * c.head_dim));
-    L.o = take(2 * L.Mpad * QD);
-    L.act = take(2 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
+    // q, o and act are split operands too: 4 bytes per value
+    L.q = take(4 * std::max(L.Mpad * QD, (size_t)L.units * L.row_tiles * 16 * c.head_dim));
+    L.o = take(4 * L.Mpad * QD);
+    L.act = take(4 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
-    L.po = L.n_parts > 1 ? take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim) : 0;
-    L.pml = L.n_parts > 1 ? take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad) : 0;
+    L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
+    L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
+    L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
+    L.blk_v = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);
     L.total = off;
     return L;
 }
@@ -291,6 +294,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.q_row_tiles = L.row_tiles;
         g.kc = kc;
         g.vc = vc;
+        g.blk_k = at<uint16_t>(ws, L.blk_k);
+        g.blk_v = at<uint16_t>(ws, L.blk_v);
         g.lengths = kv->lengths;
         g.k_blk = k;
         g.n_q_heads = nq;
@@ -310,8 +315,10 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.vc = vc;
         at_.lengths = kv->lengths;
         at_.o = at<uint16_t>(ws, L.o);
-        at_.part_o = L.n_parts > 1 ? at<float>(ws, L.po) : nullptr;
-        at_.part_ml = L.n_parts > 1 ? at<float>(ws, L.pml) : nullptr;
+        at_.blk_k = at<uint16_t>(ws, L.blk_k);
+        at_.blk_v = at<uint16_t>(ws, L.blk_v);
+        at_.part_o = at<float>(ws, L.po);
+        at_.part_ml = at<float>(ws, L.pml);
         at_.k_blk = k;
         at_.n_q_heads = nq;
         at_.n_kv_heads = nkv;
@@ -327,7 +334,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);
             HIP_TRY(launch_attention(D, L.attn_kh, L.attn_z, L.units, at_, s));
-            if (L.n_parts > 1) HIP_TRY(launch_attention_combine(D, L.units, (nq / nkv) * k, at_, s));
+            HIP_TRY(launch_attention_combine(D, L.units, (nq / nkv) * k, at_, s));
         }
 
         GemmArgs go{};

@@ -80,21 +80,29 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
             out = (r < 8) ? (y * cs - partner * sn) : (y * cs + partner * sn);
         }
         if (!ok) continue;
-        const int b = m / a.k_blk;
-        const uint16_t ob = (uint16_t)f32_to_bf16(out);
+        const int b = m / a.k_blk, jb = m - b * a.k_blk;
         if (kind == 0) {
             const int G = nq / nkv;
-            const int row = (hh % G) * a.k_blk + (m - b * a.k_blk);
-            a.q_out[q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D)] = ob;
-        } else if (pos >= a.max_len) {
-            atomicOr(a.status, DEV_CAPACITY);
-        } else if (kind == 1) {
-            const int kvh = hh - nq;
-            a.kc[((size_t)(b * nkv + kvh) * a.max_len + pos) * D + dim] = ob;
-        } else {
-            const int kvh = hh - nq - nkv;
-            a.vc[(((size_t)(b * nkv + kvh) * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;
+            const int row = (hh % G) * a.k_blk + jb;
+            store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out);
+            continue;
         }
+        // K/V: bf16 into the cache (what a commit keeps), split into the block buffer
+        // (what this pass's attention over the block's own keys reads)
+        const int kvh = hh - nq - (kind == 2 ? nkv : 0);
+        const size_t unit = (size_t)b * nkv + kvh;
+        const uint16_t ob = (uint16_t)f32_to_bf16(out);
+        const uint16_t lo = (uint16_t)f32_to_bf16(out - bf16_to_f32(ob));
+        if (kind == 1) {
+            a.blk_k[(unit * 2 * 64 + jb) * D + dim] = ob;
+            a.blk_k[((unit * 2 + 1) * 64 + jb) * D + dim] = lo;
+        } else {
+            a.blk_v[(unit * 2 * D + dim) * 64 + jb] = ob;
+            a.blk_v[((unit * 2 + 1) * D + dim) * 64 + jb] = lo;
+        }
+        if (pos >= a.max_len) atomicOr(a.status, DEV_CAPACITY);
+        else if (kind == 1) a.kc[(unit * a.max_len + pos) * D + dim] = ob;
+        else a.vc[((unit * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;
     }
 }
 
@@ -110,7 +118,7 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, f32x4_t v, int mba
         if (m < a.M && r < 8 && col < a.ffn) {
             const float gate = y, up = partner;
             const float act = gate / (1.0f + expf(-gate)) * up;
-            a.act[opnd_index(m, col, (a.ffn + 31) / 32)] = (uint16_t)f32_to_bf16(act);
+            store_split(a.act, split_index(m, col, (a.ffn + 31) / 32), act);
         }
     }
 }
@@ -150,7 +158,7 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, f32x4_t v, int mbas
         const float xn = xres[i] + v[i];
         if (ok) {
             a.x[(size_t)m * N + n] = xn;
-            a.xg_out[opnd_index(m, n, N / 32)] = (uint16_t)f32_to_bf16(xn * gn);
+            store_split(a.xg_out, split_index(m, n, N / 32), xn * gn);
         }
         float sq = ok ? xn * xn : 0.f;
         sq += __shfl_xor(sq, 1);
@@ -181,11 +189,13 @@ __device__ __forceinline__ void rms_scales(const GemmArgs& a, int m0, int rows, 
 // Normed multi-tile GEMM (M <= 16 rows).  A workgroup of NW wavefronts owns a
 // contiguous range of output tiles; wavefront w owns the reduction slice
 // [32*KS*w, 32*KS*(w+1)).  At the start each wavefront loads its slice of the
-// residual stream x, multiplies by the RMSNorm gain and keeps the bf16 operand in
-// registers for all tiles; the per-row sum of squares is reduced across the
-// wavefronts (fixed order) to the RMSNorm scale.  Weight tiles are streamed with
-// one tile in flight ahead of the one being multiplied; per tile the NW partial
-// products meet in LDS and one wavefront (rotating) runs the epilogue.
+// split operand bf16(x * gain) (hi and lo) and keeps it in registers for all
+// tiles; the per-row RMSNorm scale comes from the producer's partial sums of
+// squares.  Weights stream through one register buffer: the load of the next
+// tile's step s is issued as soon as step s of the current tile has been
+// multiplied, so one tile's worth of loads is in flight throughout.  Per tile
+// the NW partial products meet in LDS and one wavefront (rotating) runs the
+// epilogue.
 // =====================================================================================
 template <int KS, int EPI>
 __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmArgs a) {
@@ -202,24 +212,22 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     const int te = (int)((long long)T * (blockIdx.x + 1) / G);
     const int s0 = wave * KS;
 
-    // Weight tiles stream through two register buffers: the first two tiles are
-    // requested before the operand prologue, and tile t+2 as soon as tile t's
-    // MFMAs have read their registers, so two tiles are in flight throughout.
-    auto load_w = [&](int t, uint4 (&buf)[KS]) __attribute__((always_inline)) {
-        const uint4* p = a.W + ((size_t)t * a.ksteps + s0) * 64 + lane;
+    uint4 wb[KS];
+    if (tb < te) {
+        const uint4* p = a.W + ((size_t)tb * a.ksteps + s0) * 64 + lane;
 #pragma unroll
-        for (int s = 0; s < KS; ++s) buf[s] = p[(size_t)s * 64];
-    };
-    uint4 wb0[KS], wb1[KS];
-    if (tb < te) load_w(tb, wb0);
-    if (tb + 1 < te) load_w(tb + 1, wb1);
+        for (int s = 0; s < KS; ++s) wb[s] = p[(size_t)s * 64];
+    }
 
-    // operand slice: row r, columns 32*(s0+s) + 8g .. +8 of bf16(x * gain)
-    uint4 areg[KS];
+    // operand slice: row r, columns 32*(s0+s) + 8g .. +8, hi and lo
+    uint4 ah[KS], al[KS];
     const bool row_ok = r < a.M;
-    const uint16_t* ar = a.A + ((size_t)s0 * 64 + lane) * 8;
+    const uint16_t* ar = a.A + (size_t)s0 * 1024 + (size_t)lane * 8;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) areg[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 512) : uint4{0u, 0u, 0u, 0u};
+    for (int s = 0; s < KS; ++s) {
+        ah[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 1024) : uint4{0u, 0u, 0u, 0u};
+        al[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 1024 + SPLIT_LO) : uint4{0u, 0u, 0u, 0u};
+    }
     rms_scales(a, 0, 16, inv_s);
     if constexpr (EPI == EPI_QKV) {
         if (threadIdx.x < 16) {   // absolute position of block row m: P_b + j
@@ -232,30 +240,25 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     auto pos_of = [&](int i) { return pos_s[4 * g + i]; };
 
     unsigned long long key_run[4] = {0ull, 0ull, 0ull, 0ull};
-    auto finish_tile = [&](int t, int parity) __attribute__((always_inline)) {
-        f32x4_t v = red[parity][0][lane];
-        for (int w = 1; w < NW; ++w) v += red[parity][w][lane];
-        if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv, pos_of);
-        else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, 0, t, lane, inv);
-        else epi_lmhead(a, v, 0, t, lane, inv, key_run);
-    };
-
-    for (int t = tb; t < te; t += 2) {
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int t = tb; t < te; ++t) {
+        f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, accl = {0.f, 0.f, 0.f, 0.f};
+        const bool more = t + 1 < te;
+        const uint4* p = a.W + ((size_t)(t + 1) * a.ksteps + s0) * 64 + lane;
 #pragma unroll
-        for (int s = 0; s < KS; ++s) acc = mfma_16x16x32(areg[s], wb0[s], acc);
-        if (t + 2 < te) load_w(t + 2, wb0);
-        red[0][wave][lane] = acc;
+        for (int s = 0; s < KS; ++s) {
+            acc = mfma_16x16x32(ah[s], wb[s], acc);
+            accl = mfma_16x16x32(al[s], wb[s], accl);
+            if (more) wb[s] = p[(size_t)s * 64];
+        }
+        const int parity = (t - tb) & 1;
+        red[parity][wave][lane] = acc + accl;
         __syncthreads();
-        if (wave == (t - tb) % NW) finish_tile(t, 0);
-        if (t + 1 < te) {
-            acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < KS; ++s) acc = mfma_16x16x32(areg[s], wb1[s], acc);
-            if (t + 3 < te) load_w(t + 3, wb1);
-            red[1][wave][lane] = acc;
-            __syncthreads();
-            if (wave == (t + 1 - tb) % NW) finish_tile(t + 1, 1);
+        if (wave == (t - tb) % NW) {
+            f32x4_t v = red[parity][0][lane];
+            for (int w = 1; w < NW; ++w) v += red[parity][w][lane];
+            if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv, pos_of);
+            else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, 0, t, lane, inv);
+            else epi_lmhead(a, v, 0, t, lane, inv, key_run);
         }
     }
 
@@ -305,20 +308,25 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // Streamed GEMM: out[m][n] = sum_k A[m][k] W[n][k] for 16*MT rows x 16*CT columns per
 // workgroup; the NW wavefronts split the reduction, each streaming its slice of the
 // weights and of the bf16 activations with one batch in flight ahead of the MFMAs.
-// Used for the O and down projections (residual epilogue) and, for M > 16, for
-// every projection (the per-row RMSNorm scale is then formed in the prologue).
+// Every operand is split (two MFMAs per weight operand).  Used for the O and down
+// projections (residual epilogue) and, for M > 16, for every projection (the
+// per-row RMSNorm scale is then formed in the prologue).
 // =====================================================================================
-template <int MT, int CT>
+template <int MT, int CT, bool SPLIT>
 struct Batch {
-    static constexpr int U = (CT + MT <= 2) ? 8 : ((CT + MT <= 5) ? 4 : 2);
+    static constexpr int OPS = CT + MT * (SPLIT ? 2 : 1);   // operand quads per k-step
+    static constexpr int U = (OPS <= 3) ? 8 : ((OPS <= 5) ? 4 : 2);
     uint4 w[U][CT];
     uint4 x[U][MT];
+    uint4 xl[SPLIT ? U : 1][SPLIT ? MT : 1];
 };
 
 template <int MT, int CT, int NW, int EPI>
 __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
-    typedef Batch<MT, CT> B;
+    constexpr bool SPLIT = true;
+    typedef Batch<MT, CT, SPLIT> B;
     constexpr int U = B::U;
+    constexpr int BSTRIDE = SPLIT ? 1024 : 512;   // elements per (row tile, k-step) block
     __shared__ f32x4_t red[NW][MT * CT][64];
     __shared__ unsigned long long key_s[16 * MT];
     __shared__ float inv_s[16 * MT];
@@ -344,14 +352,20 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         aok[mt] = m0 + mt * 16 + r < a.M;
-        ap[mt] = a.A + ((size_t)(blockIdx.y * MT + mt) * a.ksteps * 64 + lane) * 8;
+        ap[mt] = a.A + (size_t)(blockIdx.y * MT + mt) * a.ksteps * BSTRIDE + (size_t)lane * 8;
     }
 
-    f32x4_t acc[MT][CT];
+    f32x4_t acc[MT][CT], accl[SPLIT ? MT : 1][SPLIT ? CT : 1];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if constexpr (SPLIT) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) accl[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
 
     // residual values for the epilogue of this wavefront's first tile, fetched up front
     float xres[4] = {0.f, 0.f, 0.f, 0.f};
@@ -377,8 +391,11 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
             for (int ct = 0; ct < CT; ++ct) buf.w[u][ct] = in ? wp[ct][(size_t)ss * 64] : zero4;
             const int kcol = ss * 32 + 8 * g;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                buf.x[u][mt] = (in && aok[mt] && kcol < a.K) ? *(const uint4*)(ap[mt] + (size_t)ss * 512) : zero4;
+            for (int mt = 0; mt < MT; ++mt) {
+                const bool ok = in && aok[mt] && kcol < a.K;
+                buf.x[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE) : zero4;
+                if constexpr (SPLIT) buf.xl[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE + SPLIT_LO) : zero4;
+            }
         }
     };
     auto compute = [&](const B& buf) __attribute__((always_inline)) {
@@ -387,7 +404,10 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = mfma_16x16x32(buf.x[u][mt], buf.w[u][ct], acc[mt][ct]);
+                for (int ct = 0; ct < CT; ++ct) {
+                    acc[mt][ct] = mfma_16x16x32(buf.x[u][mt], buf.w[u][ct], acc[mt][ct]);
+                    if constexpr (SPLIT) accl[mt][ct] = mfma_16x16x32(buf.xl[u][mt], buf.w[u][ct], accl[mt][ct]);
+                }
     };
 
     B b0, b1;
@@ -400,6 +420,12 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         compute(b1);
     }
 
+    if constexpr (SPLIT) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) acc[mt][ct] += accl[mt][ct];
+    }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -486,12 +512,18 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
 // =====================================================================================
 // Block-masked GQA attention.  Workgroup = (key split, sequence x KV head, row slice);
 // one compute wavefront per 16 query rows of the GQA group (rows = heads of the
-// group x block rows).  Keys stream through LDS in stages of 64 (K rows and the
-// cache's transposed V tile, XOR-swizzled for conflict-free operand reads), double
-// buffered: the next stage's global loads are in flight while the current one is
-// multiplied.  S^T = K Q^T on MFMA puts one query row per lane column, so a row's
-// softmax statistics live in lanes r, r+16, r+32, r+48 and P^T is already the B
-// operand of O^T = V^T P^T.  Online softmax in base 2, fp32.
+// group x block rows).  The committed prefix [0, P) is cut into key splits that
+// read the bf16 cache; one more workgroup per (unit, row slice), the block part,
+// covers the block's own k keys (causal or bidirectional per the mode) from the
+// split K/V the QKV epilogue left in the workspace, so this pass sees its own keys
+// and values at about 16 significant bits while the cache keeps bf16.  Keys stream
+// through LDS in stages of 64 (K rows and the transposed V tile, XOR-swizzled for
+// conflict-free operand reads), double buffered: the next stage's global loads are
+// in flight while the current one is multiplied.  S^T = K Q^T on MFMA puts one
+// query row per lane column, so a row's softmax statistics live in lanes r, r+16,
+// r+32, r+48 and P^T is already the B operand of O^T = V^T P^T.  Queries and P are
+// split operands.  Online softmax in base 2, fp32; every workgroup writes one
+// partial (max, sum, unnormalised output) per row for the merge.
 // =====================================================================================
 template <int D>
 struct AttnCfg {
@@ -532,6 +564,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, unit = blockIdx.y;
+    const bool blockpart = split == a.n_splits;   // the block's own keys, read in split form
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv;
     const int k = a.k_blk, R = G * k;
@@ -544,13 +577,13 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
 
     int P = a.lengths[b];
     P = P < 0 ? 0 : (P > a.max_len ? a.max_len : P);
-    const int T = min(P + k, a.max_len);
-    const int kbeg = split * a.chunk;
-    const int kend = min(kbeg + a.chunk, T);
+    // prefix splits cover committed keys [kbeg, kend) of [0, P); the block part covers [P, P + k)
+    const int kbeg = blockpart ? P : split * a.chunk;
+    const int kend = blockpart ? P + k : min(kbeg + a.chunk, P);
     const bool bidir_row = (a.mode == 1) && (j >= a.bidir_from);
 
     const size_t head_off = (size_t)(b * nkv + kvh) * a.max_len * D;
-    const uint16_t* kbase = a.kc + head_off;
+    const uint16_t* kbase = a.kc + head_off;   // where gload reads stages from
     const uint16_t* vbase = a.vc + head_off;
 
     // per-thread stage chunks: global offsets within a stage and LDS slots (swizzled)
@@ -606,11 +639,14 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     }
 
     const uint4 zero4 = {0u, 0u, 0u, 0u};
-    uint4 qb[DC];
+    uint4 qb[DC], ql[DC];   // split queries: hi and lo operands
     {
-        const uint16_t* qp = a.q + ((size_t)((unit * a.row_tiles + rt) * DC) * 64 + lane) * 8;
+        const uint16_t* qp = a.q + ((size_t)((unit * a.row_tiles + rt) * DC * 2) * 64 + lane) * 8;
 #pragma unroll
-        for (int c = 0; c < DC; ++c) qb[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 512) : zero4;
+        for (int c = 0; c < DC; ++c) {
+            qb[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 1024) : zero4;
+            ql[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 1024 + SPLIT_LO) : zero4;
+        }
     }
 
     f32x4_t acc[DT];
@@ -620,14 +656,23 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     // so the accumulators are rescaled rarely (any reference gives the same ratio).
     float m_ref = -INFINITY, l_part = 0.f;
 
-    auto compute = [&](int kb, int buf) __attribute__((always_inline)) {
+    // kb: first key of the stage.  lo_slot: the block part keeps the lo halves of
+    // the block's keys and values in the second stage slot.
+    auto compute = [&](int kb, int buf, bool lo_slot) __attribute__((always_inline)) {
         if (!computes) return;
-        f32x4_t s[TPW];
+        f32x4_t s[TPW], sl[TPW];
 #pragma unroll
         for (int tt = 0; tt < TPW; ++tt) {
             s[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            sl[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < DC; ++c) s[tt] = mfma_16x16x32(lds[buf * C::CHUNKS + koff[tt][c]], qb[c], s[tt]);
+            for (int c = 0; c < DC; ++c) {
+                const uint4 kop = lds[buf * C::CHUNKS + koff[tt][c]];
+                s[tt] = mfma_16x16x32(kop, qb[c], s[tt]);
+                sl[tt] = mfma_16x16x32(kop, ql[c], sl[tt]);
+                if (lo_slot) sl[tt] = mfma_16x16x32(lds[C::CHUNKS + koff[tt][c]], qb[c], sl[tt]);
+            }
+            s[tt] += sl[tt];
         }
         const bool edge = (kb + 64 > P) || (kb + 64 > kend);   // stage touches the block or the split end
         float sv[4 * TPW];
@@ -667,42 +712,58 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         for (int kk = 0; kk < TPW / 2; ++kk) {
             const int ks = (TPW / 2) * kh + kk;          // 32-key PV step within the stage
             // slot jj of lane group g <-> key kb + 32ks + 8g + jj
-            const float* pp = p + 8 * kk;
-            uint4 pop = {pack_bf16x2(pp[0], pp[1]), pack_bf16x2(pp[2], pp[3]), pack_bf16x2(pp[4], pp[5]),
-                         pack_bf16x2(pp[6], pp[7])};
-            if (m_ref == -INFINITY) pop = zero4;
+            uint4 pop, pol;                               // P^T as split operands
+            split8(p + 8 * kk, pop, pol);
+            if (m_ref == -INFINITY) pop = pol = zero4;
             const int key0 = kb + 32 * ks + 8 * g;
             const bool vmask = edge && (key0 + 8 > kend);  // V rows past the valid keys may hold anything
+            auto masked = [&](uint4 vop) __attribute__((always_inline)) {
+                if (!vmask) return vop;
+                uint32_t w[4] = {vop.x, vop.y, vop.z, vop.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (key0 + 2 * e < kend ? (w[e] & 0xFFFFu) : 0u) | (key0 + 2 * e + 1 < kend ? (w[e] & 0xFFFF0000u) : 0u);
+                return uint4{w[0], w[1], w[2], w[3]};
+            };
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
-                uint4 vop = lds[buf * C::CHUNKS + C::KCHUNKS + voff[kk][dt]];
-                if (vmask) {
-                    uint32_t w[4] = {vop.x, vop.y, vop.z, vop.w};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        w[e] = (key0 + 2 * e < kend ? (w[e] & 0xFFFFu) : 0u) | (key0 + 2 * e + 1 < kend ? (w[e] & 0xFFFF0000u) : 0u);
-                    vop = uint4{w[0], w[1], w[2], w[3]};
-                }
+                const uint4 vop = masked(lds[buf * C::CHUNKS + C::KCHUNKS + voff[kk][dt]]);
                 acc[dt] = mfma_16x16x32(vop, pop, acc[dt]);
+                acc[dt] = mfma_16x16x32(vop, pol, acc[dt]);
+                if (lo_slot) acc[dt] = mfma_16x16x32(masked(lds[C::CHUNKS + C::KCHUNKS + voff[kk][dt]]), pop, acc[dt]);
             }
         }
     };
 
-    // stages of 64 keys; two stages in flight in registers while one is multiplied from LDS
-    const int nst = kend > kbeg ? (kend - kbeg + 63) / 64 : 0;
-    Stage n1{}, n2{};
-    if (nst > 0) {
-        lstore(gload(kbeg), 0);
-        if (nst > 1) n1 = gload(kbeg + 64);
-        if (nst > 2) n2 = gload(kbeg + 128);
-    }
-    __syncthreads();
-    for (int st = 0; st < nst; ++st) {
-        compute(kbeg + 64 * st, st & 1);
-        if (st + 1 < nst) lstore(n1, (st + 1) & 1);
-        n1 = n2;
-        if (st + 3 < nst) n2 = gload(kbeg + 64 * (st + 3));
+    if (blockpart) {
+        // one stage (k <= 64): hi halves into slot 0, lo halves into slot 1
+        const size_t kv_unit = (size_t)unit * 2 * 64 * D;
+        kbase = a.blk_k + kv_unit;
+        vbase = a.blk_v + kv_unit;
+        lstore(gload(0), 0);
+        kbase += 64 * D;
+        vbase += 64 * D;
+        lstore(gload(0), 1);
         __syncthreads();
+        compute(kbeg, 0, true);
+        __syncthreads();
+    } else {
+        // stages of 64 keys; two stages in flight in registers while one is multiplied from LDS
+        const int nst = kend > kbeg ? (kend - kbeg + 63) / 64 : 0;
+        Stage n1{}, n2{};
+        if (nst > 0) {
+            lstore(gload(kbeg), 0);
+            if (nst > 1) n1 = gload(kbeg + 64);
+            if (nst > 2) n2 = gload(kbeg + 128);
+        }
+        __syncthreads();
+        for (int st = 0; st < nst; ++st) {
+            compute(kbeg + 64 * st, st & 1, false);
+            if (st + 1 < nst) lstore(n1, (st + 1) & 1);
+            n1 = n2;
+            if (st + 3 < nst) n2 = gload(kbeg + 64 * (st + 3));
+            __syncthreads();
+        }
     }
 
     float l_tot = l_part + __shfl_xor(l_part, 16);
@@ -735,19 +796,6 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         m_ref = mm;
     }
     if (!computes) return;
-    const int HD = a.n_q_heads * D;
-    if (a.n_parts == 1) {
-        if (row_ok) {
-            const int m = b * k + j, head = kvh * G + row / k;
-            const float inv = 1.0f / l_tot;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    a.o[opnd_index(m, head * D + 16 * dt + 4 * g + i, HD / 32)] = (uint16_t)f32_to_bf16(acc[dt][i] * inv);
-        }
-        return;
-    }
     const size_t pbase = ((size_t)unit * a.n_parts + split) * a.rows_pad + row;
     float* po = a.part_o + pbase * D;
 #pragma unroll
@@ -755,7 +803,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     if (g == 0) *(float2*)(a.part_ml + pbase * 2) = float2{m_ref, l_tot};
 }
 
-// Merge of the key splits: one workgroup per (unit, query row), one thread per head dim.
+// Merge of the partials (prefix splits + block part): one workgroup per (unit, query
+// row), one thread per head dim; writes the split attention output.
 template <int D>
 __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     __shared__ float wsh[256];
@@ -811,11 +860,11 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     }
     for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)sp * a.rows_pad) * D + d];
     const int hl = rw / k, j = rw % k;
-    a.o[opnd_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32)] = (uint16_t)f32_to_bf16(num * inv_den);
+    store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den);
 }
 
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
-    const dim3 grid(a.n_splits, units, zslices);
+    const dim3 grid(a.n_splits + 1, units, zslices);   // prefix splits + the block part
     if (head_dim == 128 && kh == 2) attention_kernel<128, 2><<<grid, 512, 0, s>>>(a);
     else if (head_dim == 128 && kh == 1) attention_kernel<128, 1><<<grid, 512, 0, s>>>(a);
     else if (head_dim == 64 && kh == 2) attention_kernel<64, 2><<<grid, 512, 0, s>>>(a);
@@ -858,20 +907,23 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
             const uint4 w = *(const uint4*)(e + col);
             const uint4 gg = *(const uint4*)(a.gain + col);
             const uint32_t ew[4] = {w.x, w.y, w.z, w.w}, gw[4] = {gg.x, gg.y, gg.z, gg.w};
-            float xv[8];
-            uint32_t xb[4];
+            float xv[8], xgv[8];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 xv[2 * q] = bf16_to_f32(ew[q] & 0xFFFFu);
                 xv[2 * q + 1] = bf16_to_f32(ew[q] >> 16);
-                xb[q] = f32_to_bf16(xv[2 * q] * bf16_to_f32(gw[q] & 0xFFFFu)) |
-                        (f32_to_bf16(xv[2 * q + 1] * bf16_to_f32(gw[q] >> 16)) << 16);
+                xgv[2 * q] = xv[2 * q] * bf16_to_f32(gw[q] & 0xFFFFu);
+                xgv[2 * q + 1] = xv[2 * q + 1] * bf16_to_f32(gw[q] >> 16);
             }
 #pragma unroll
             for (int q = 0; q < 8; ++q) ss += xv[q] * xv[q];
             *(float4*)(a.x + row + col) = float4{xv[0], xv[1], xv[2], xv[3]};
             *(float4*)(a.x + row + col + 4) = float4{xv[4], xv[5], xv[6], xv[7]};
-            *(uint4*)(a.xg + opnd_index(m, col, a.hidden / 32)) = uint4{xb[0], xb[1], xb[2], xb[3]};
+            uint4 hi, lo;
+            split8(xgv, hi, lo);
+            const size_t xi = split_index(m, col, a.hidden / 32);
+            *(uint4*)(a.xg + xi) = hi;
+            *(uint4*)(a.xg + xi + SPLIT_LO) = lo;
         }
         a.part_ss[(size_t)m * chunks + c] = ss;
     }

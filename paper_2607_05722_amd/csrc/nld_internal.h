@@ -45,21 +45,44 @@ __device__ __forceinline__ int32_t argmax_key_index(unsigned long long key) {
     return (int32_t)(0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull));
 }
 
-// Activation operands (the A side of every projection) are stored in MFMA
-// operand order: rows in tiles of 16, columns in steps of 32; tile mt, step s
-// is one 1 KiB block whose 16-byte lane l holds A[16mt + l%16][32s + 8(l/16) .. +8],
-// so a wavefront fetches one operand with one contiguous 1 KiB load.
-__host__ __device__ __forceinline__ size_t opnd_index(int m, int k, int ksteps) {
-    return ((size_t)((m >> 4) * ksteps + (k >> 5)) * 64 + (size_t)((((k & 31) >> 3) << 4) + (m & 15))) * 8 + (k & 7);
+// Activation operands (the A side of every projection) are split and stored in
+// MFMA operand order.  Split: a value a is carried as two bfloat16 numbers,
+// hi = bf16(a) and lo = bf16(a - hi); against an exact bf16 weight, hi*w + lo*w
+// (two MFMAs, fp32 accumulation) keeps about 16 significant bits of a instead of
+// 8.  Operand order: rows in tiles of 16, columns in steps of 32; tile mt, step s
+// is a 1 KiB hi block whose 16-byte lane l holds A[16mt + l%16][32s + 8(l/16) .. +8],
+// followed by the lo block of the same shape, so a wavefront fetches each half
+// of an operand with one contiguous 1 KiB load.  Returns the index of the hi value.
+__host__ __device__ __forceinline__ size_t split_index(int m, int k, int ksteps) {
+    return ((size_t)(((m >> 4) * ksteps + (k >> 5)) * 2) * 64 + (size_t)((((k & 31) >> 3) << 4) + (m & 15))) * 8 + (k & 7);
+}
+constexpr int SPLIT_LO = 512;   // element offset of a lo value from its hi value
+
+__device__ __forceinline__ void store_split(uint16_t* p, size_t hi_index, float v) {
+    const uint32_t h = f32_to_bf16(v);
+    p[hi_index] = (uint16_t)h;
+    p[hi_index + SPLIT_LO] = (uint16_t)f32_to_bf16(v - bf16_to_f32(h));
+}
+
+// eight floats -> hi and lo operand quads (element e in bits 16(e%2) of word e/2)
+__device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        h[q] = pack_bf16x2(v[2 * q], v[2 * q + 1]);
+        l[q] = pack_bf16x2(v[2 * q] - bf16_to_f32(h[q] & 0xFFFFu), v[2 * q + 1] - bf16_to_f32(h[q] >> 16));
+    }
+    hi = uint4{h[0], h[1], h[2], h[3]};
+    lo = uint4{l[0], l[1], l[2], l[3]};
 }
 
 // ---------------------------------------------------------------- kernel arguments
 enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
-    // A operand: bf16 activations in operand order (opnd_index with `ksteps`).
+    // A operand: split bf16 activations in operand order (split_index with `ksteps`).
     // For the projections whose input is RMSNorm(x) (QKV, gate/up, LM head) A is
-    // bf16(x * gain), written by the kernel that produced x, and part_ss holds that
+    // x * gain, written by the kernel that produced x, and part_ss holds that
     // producer's sums of x^2 over 16-column chunks ([M][n_ss]); the consumer turns
     // them into 1/rms per row.
     const uint16_t* A;
@@ -73,21 +96,23 @@ struct GemmArgs {
     int ksteps;          // ceil(K / 32)
     // EPI_RESID: x += A W^T, then the next RMSNorm's operand and statistics
     float* x;
-    uint16_t* xg_out;          // bf16(x * gain_next), operand order with N/32 steps
+    uint16_t* xg_out;          // split x * gain_next, split_index with N/32 steps
     const uint16_t* gain_next;
     float* part_ss_out;        // [M][N/16]
     // EPI_QKV
-    uint16_t* q_out;     // bf16 queries in the attention's operand order (q_index)
+    uint16_t* q_out;     // split bf16 queries in the attention's operand order (q_index)
     int q_row_tiles;     // query-row tiles of 16 per (sequence, KV head)
     uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
     uint16_t* vc;        // this layer's V cache [batch][n_kv_heads][max_len/64][head_dim][64]
+    uint16_t* blk_k;     // the block's own keys, split: [unit][hi, lo][64 rows][head_dim]
+    uint16_t* blk_v;     // the block's own values, split: [unit][hi, lo][head_dim][64 rows]
     const int32_t* lengths;
     int k_blk;
     int n_q_heads, n_kv_heads, head_dim, max_len;
     double inv_freq[64];  // RoPE frequencies base^(-2i/head_dim), i < head_dim/2 (computed on the host in fp64)
     uint32_t* status;
     // EPI_SWIGLU
-    uint16_t* act;       // bf16 silu(gate) * up, operand order with ceil(ffn/32) steps
+    uint16_t* act;       // split bf16 silu(gate) * up, split_index with ceil(ffn/32) steps
     int ffn;
     // EPI_LMHEAD
     float* logits;                   // optional f32 [M][vocab]
@@ -98,22 +123,25 @@ struct GemmArgs {
 
 // Queries are stored per (sequence b, KV head) unit with the unit's rows
 // (row = local head * k + block row j) in tiles of 16 and head dims in steps of
-// 32, in MFMA operand order: one 1 KiB block per (row tile, step).
+// 32, in MFMA operand order, split: one 1 KiB hi block and its 1 KiB lo block per
+// (row tile, step).  Returns the index of the hi value.
 __host__ __device__ __forceinline__ size_t q_index(int unit, int row, int d, int row_tiles, int D) {
-    return ((size_t)((unit * row_tiles + (row >> 4)) * (D >> 5) + (d >> 5)) * 64 + (size_t)((((d & 31) >> 3) << 4) + (row & 15))) * 8 + (d & 7);
+    return ((size_t)(((unit * row_tiles + (row >> 4)) * (D >> 5) + (d >> 5)) * 2) * 64 + (size_t)((((d & 31) >> 3) << 4) + (row & 15))) * 8 + (d & 7);
 }
 
 struct AttnArgs {
-    const uint16_t* q;   // bf16 queries (q_index)
+    const uint16_t* q;   // split bf16 queries (q_index)
     const uint16_t* kc;  // this layer's K cache
     const uint16_t* vc;  // this layer's V cache (64-position transposed tiles)
+    const uint16_t* blk_k;  // the block's keys and values in split form (GemmArgs::blk_k, blk_v)
+    const uint16_t* blk_v;
     const int32_t* lengths;
-    uint16_t* o;         // bf16 attention output, operand order with n_q_heads*D/32 steps
-    float* part_o;       // [units][n_splits][rows_pad][D]
-    float* part_ml;      // [units][n_splits][rows_pad][2]
+    uint16_t* o;         // split bf16 attention output, split_index with n_q_heads*D/32 steps
+    float* part_o;       // [units][n_parts][rows_pad][D]
+    float* part_ml;      // [units][n_parts][rows_pad][2]
     int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
     int row_tiles;       // query-row tiles of 16 per unit (GQA group size x k / 16, rounded up)
-    int n_parts;         // partial results per (unit, row): n_splits x key halves
+    int n_parts;         // partial results per (unit, row): n_splits prefix splits + the block part
     float scale_log2;    // log2(e) / sqrt(D)
 };
 
@@ -126,7 +154,7 @@ struct EmbedArgs {
     const uint16_t* embed;
     const uint16_t* gain;   // first layer's attention RMSNorm gain
     float* x;
-    uint16_t* xg;           // operand order with hidden/32 steps
+    uint16_t* xg;           // split x * gain, split_index with hidden/32 steps
     float* part_ss;         // [M][hidden/16]
     uint32_t* status;
 };

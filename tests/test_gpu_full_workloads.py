@@ -1,0 +1,154 @@
+"""GPU parity at the full workload sizes, on the launch configuration the benchmark times.
+
+The oracle cannot afford every sequence of the large batches, so it recomputes a
+sample of sequences (every sequence's block is independent of the others) and the
+comparison covers those sequences' logits, argmax and acceptance.  All inputs come
+from the seeded generator; the oracle never sees a GPU result.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import nld_oracle as O
+from synth.workloads import LazyWeights, ModelShape, WORKLOADS, prefix_kv, tokens as synth_tokens
+
+from gpu_common import check_argmax, log, rel_err
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def R():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_05722_amd import runtime
+    return runtime
+
+
+class SubBatch:
+    """Prefix K/V of a subset of a batch's sequences, drawn from the full-batch generator."""
+
+    def __init__(self, wl, seqs):
+        self.wl, self.seqs = wl, list(seqs)
+        self.lengths = wl.prefix_lengths()
+
+    def fill(self, okv, cache_gpu, max_prefix):
+        shape = self.wl.shape
+        for l in range(shape.n_layers):
+            kb, vb = prefix_kv(shape, self.wl.seed, l, self.wl.batch, max_prefix)
+            cache_gpu.load_prefix(l, kb, vb)
+            okv.set_prefix_bf16(l, kb[self.seqs], vb[self.seqs], self.lengths[self.seqs])
+            del kb, vb
+
+
+def _setup(R, name, seqs):
+    wl = WORKLOADS[name]
+    shape, k, B = wl.shape, wl.k_values[0], wl.batch
+    plens = wl.prefix_lengths()
+    maxp = int(plens.max())
+    max_len = (maxp + 2 * k + 63) // 64 * 64
+    src = LazyWeights(shape, wl.seed, keep=True)
+    log("%s: building model" % name)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, B, max_len)
+    okv = O.OracleKV(shape, len(seqs), max_len, np.float32)
+    SubBatch(wl, seqs).fill(okv, cache, maxp)
+    cache.set_lengths(plens)
+    w = O.OracleWeights(shape, src, np.float32)
+    return wl, shape, k, B, plens, max_len, model, cache, okv, w
+
+
+def test_8b_full_self_speculation_step(R):
+    """36-layer 8B stack, batch 1, prefix 4096, k=16: draft pass, verify pass, acceptance and commit."""
+    wl, shape, k, B, plens, max_len, model, cache, okv, w = _setup(R, "8b", [0])
+    anchor = synth_tokens(shape, wl.seed, "test.8b.anchor", (1,))
+    ws = R.Workspace(model, B, k, max_len)
+    a_g = torch.from_numpy(anchor).cuda()
+    d_g, dl = R.draft(model, cache, ws, a_g, k, want_logits=True)
+    gd = d_g.cpu().numpy()
+    log("8b: oracle draft pass")
+    od, ref_d = O.draft_pass(w, okv, anchor, k)
+    e_d = rel_err(dl.cpu().numpy(), ref_d)
+    log("8b: draft rel err %.3e" % e_d)
+    assert e_d <= TOL
+    # draft tokens: argmax of GPU draft logits; equal to the oracle's except on near-ties
+    near = check_argmax(gd, dl.cpu().numpy()[:, 1:], ref_d[:, 1:], e_d * np.max(np.abs(ref_d)))
+    log("8b: near-tie draft rows differing: %s" % near)
+    # verify on the oracle's drafts (GPU and oracle consume the same drafts)
+    drafts = od.astype(np.int32)
+    out = R.verify_accept(model, cache, ws, a_g, torch.from_numpy(drafts).cuda(), k, want_logits=True)
+    log("8b: oracle verify pass")
+    a, ref_v, nk, nv = O.verify_pass(w, okv, anchor, drafts)
+    g_v = out["logits"].cpu().numpy()
+    e_v = rel_err(g_v, ref_v)
+    log("8b: verify rel err %.3e" % e_v)
+    assert e_v <= TOL
+    # acceptance is bit-exact given the GPU's own argmax; equal to the oracle's away from near-ties
+    g_a = np.argmax(g_v, axis=-1).astype(np.int32)
+    L, committed, bonus = O.accept(drafts[0], g_a[0])
+    assert int(out["accept_len"].cpu()[0]) == L
+    assert out["committed"][0].cpu().tolist()[:L + 1] == committed
+    assert int(out["next_anchor"].cpu()[0]) == bonus
+    assert int(cache.lengths.cpu()[0]) == int(plens[0]) + L + 1
+    check_argmax(g_a, g_v, ref_v, e_v * np.max(np.abs(ref_v)))
+    kg, vg = cache.read_kv(shape.n_layers - 1, int(plens[0]), int(plens[0]) + k)
+    assert rel_err(O.bf16_bits_to_float(kg), nk[-1]) < TOL
+    assert rel_err(O.bf16_bits_to_float(vg), nv[-1]) < TOL
+    assert R.read_device_status(ws) == 0
+
+
+def test_8b_batch32_ragged_verify(R):
+    """36-layer 8B, batch 32 with ragged prefixes in [512, 8192], k=16, verify mask: sequences with the
+    shortest and the longest prefix are recomputed by the oracle."""
+    wl = WORKLOADS["8b_batch32"]
+    plens = wl.prefix_lengths()
+    seqs = [int(np.argmin(plens)), int(np.argmax(plens))]
+    wl, shape, k, B, plens, max_len, model, cache, okv, w = _setup(R, "8b_batch32", seqs)
+    blk = synth_tokens(shape, wl.seed, "test.8b_batch32.block", (B, k))
+    ws = R.Workspace(model, B, k, max_len)
+    logits, am = R.block_forward(model, cache, ws, torch.from_numpy(blk).cuda(), R.VERIFY)
+    g = logits.cpu().numpy()[seqs]
+    log("8b_batch32: oracle verify pass over sequences %s (prefixes %s)" % (seqs, plens[seqs].tolist()))
+    ref, _, _ = O.block_forward(w, okv, blk[seqs], O.VERIFY)
+    e = rel_err(g, ref)
+    log("8b_batch32: rel err %.3e" % e)
+    assert e <= TOL
+    check_argmax(am.cpu().numpy()[seqs], g, ref, e * np.max(np.abs(ref)))
+    # every sequence's argmax is the first maximum of its own logits
+    assert np.array_equal(am.cpu().numpy(), np.argmax(logits.cpu().numpy(), axis=-1))
+    assert R.read_device_status(ws) == 0
+
+
+def test_14b_self_speculation_step(R):
+    """40-layer 14B shape, batch 8, prefix 16384, k=32: draft + verify + acceptance; sequences 0 and 5
+    are recomputed by the oracle."""
+    seqs = [0, 5]
+    wl, shape, k, B, plens, max_len, model, cache, okv, w = _setup(R, "14b", seqs)
+    anchor = synth_tokens(shape, wl.seed, "test.14b.anchor", (B,))
+    ws = R.Workspace(model, B, k, max_len)
+    a_g = torch.from_numpy(anchor).cuda()
+    d_g, dl = R.draft(model, cache, ws, a_g, k, want_logits=True)
+    log("14b: oracle draft pass")
+    od, ref_d = O.draft_pass(w, okv, anchor[seqs], k)
+    e_d = rel_err(dl.cpu().numpy()[seqs], ref_d)
+    log("14b: draft rel err %.3e" % e_d)
+    assert e_d <= TOL
+    drafts = synth_tokens(shape, wl.seed, "test.14b.drafts", (B, k - 1))
+    drafts[seqs] = od
+    out = R.verify_accept(model, cache, ws, a_g, torch.from_numpy(drafts).cuda(), k, want_logits=True)
+    log("14b: oracle verify pass")
+    a, ref_v, _, _ = O.verify_pass(w, okv, anchor[seqs], drafts[seqs])
+    g_v = out["logits"].cpu().numpy()
+    e_v = rel_err(g_v[seqs], ref_v)
+    log("14b: verify rel err %.3e" % e_v)
+    assert e_v <= TOL
+    g_a = np.argmax(g_v, axis=-1).astype(np.int32)
+    for b in range(B):
+        L, committed, bonus = O.accept(drafts[b], g_a[b])
+        assert int(out["accept_len"].cpu()[b]) == L
+        assert out["committed"][b].cpu().tolist()[:L + 1] == committed
+        assert int(cache.lengths.cpu()[b]) == int(plens[b]) + L + 1
+    check_argmax(g_a[seqs], g_v[seqs], ref_v, e_v * np.max(np.abs(ref_v)))
+    assert R.read_device_status(ws) == 0
