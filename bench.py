@@ -66,39 +66,81 @@ def blas_threads():
         return os.cpu_count()
 
 
-def cpu_baseline(wl, k, sample_layers=(2, 4)):
-    """Time the CPU oracle's verify pass on the first few layers + LM head; extrapolate linearly in layers."""
+def cpu_baseline(wl, k, min_seconds=10.0, max_passes=8):
+    """Time the CPU oracle's verify pass over the full model (batch 1 of the workload, every layer + LM head).
+
+    Passes repeat until at least `min_seconds` of CPU work have been timed (two passes at least)."""
     from oracle import nld_oracle as O
-    from synth.workloads import LazyWeights, ModelShape, prefix_kv, tokens
+    from synth.workloads import LazyWeights, prefix_kv, tokens
 
     shape = wl.shape
     P = int(wl.prefix_lengths()[0])
-    times = {}
-    for nl in sample_layers:
-        sub = ModelShape(**{**shape.__dict__, "n_layers": nl})
-        src = LazyWeights(sub, wl.seed, keep=True)
-        for l in range(nl):
-            src.layer(l)
-        _ = src.embed, src.lm_head
-        w = O.OracleWeights(sub, src, np.float32)
-        kv = O.OracleKV(sub, 1, P + k, np.float32)
-        for l in range(nl):
-            kb, vb = prefix_kv(shape, wl.seed, l, 1, P)
-            kv.set_prefix_bf16(l, kb, vb, [P])
-        blk = tokens(shape, wl.seed, "bench.cpu.block", (1, k))
+    src = LazyWeights(shape, wl.seed, keep=True)
+    for l in range(shape.n_layers):
+        src.layer(l)
+    _ = src.embed, src.lm_head
+    w = O.OracleWeights(shape, src, np.float32)
+    kv = O.OracleKV(shape, 1, P + k, np.float32)
+    for l in range(shape.n_layers):
+        kb, vb = prefix_kv(shape, wl.seed, l, 1, P)
+        kv.set_prefix_bf16(l, kb[:1], vb[:1], [P])
+    blk = tokens(shape, wl.seed, "bench.cpu.block", (1, k))
+    times = []
+    while len(times) < max_passes and (len(times) < 2 or sum(times) < min_seconds):
         t0 = time.perf_counter()
         O.block_forward(w, kv, blk, O.VERIFY)
-        times[nl] = time.perf_counter() - t0
-        log("oracle pass with %d layers + LM head: %.2f s" % (nl, times[nl]))
-    a, b = sample_layers
-    per_layer = max((times[b] - times[a]) / (b - a), 1e-9)
-    t_pass = times[b] + (shape.n_layers - b) * per_layer
+        times.append(time.perf_counter() - t0)
+        log("oracle verify pass %d: %.2f s" % (len(times), times[-1]))
+    total = sum(times)
     return {
-        "value": round(k / t_pass, 4), "unit": "block tokens/s", "cores": int(blas_threads()), "kind": "oracle",
-        "sample": "fp32 numpy oracle, one verify pass (batch 1, k=%d, prefix %d) over the first %d and %d of %d "
-                  "layers + LM head (%.1f s, %.1f s); full pass extrapolated linearly in layers: %.1f s"
-                  % (k, P, a, b, shape.n_layers, times[a], times[b], t_pass),
+        "value": round(k * len(times) / total, 4), "unit": "block tokens/s", "cores": int(blas_threads()),
+        "kind": "oracle",
+        "sample": "fp32 numpy oracle, %d full verify passes (batch 1 of the workload, k=%d, prefix %d, all %d layers "
+                  "+ LM head), %.1f s in total" % (len(times), k, P, shape.n_layers, total),
     }
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("kernels.hip", "nld_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_05722_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when that summary is
+    missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "%s_8b_hbm_traffic.md" % kernel)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                key, val = line[2:].split(": ", 1)
+                vals[key.strip()] = val.strip().strip("`")
+    if vals.get("kernel sources sha256[:16]") != kernel_source_digest():
+        return None
+    try:
+        return int(vals["HBM bytes per launch (read + write)"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib, reps=3):
+    """Plain device-to-device copies of a known size, for scaling the counters of a --pmc run."""
+    import torch
+    n = mib * 1024 * 1024 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("copy calibration: %d x copy of %d MiB (read %d KiB, write %d KiB per dispatch)" % (reps, mib, mib * 1024,
+                                                                                             mib * 1024))
+    del src, dst
 
 
 def main():
@@ -109,6 +151,8 @@ def main():
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run plain copies of this many MiB (reference dispatches for counter runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1).", file=sys.stderr)
@@ -119,6 +163,8 @@ def main():
     from paper_2607_05722_amd import runtime as R
     from synth.workloads import LazyWeights, WORKLOADS, prefix_kv, tokens
 
+    if args.copy_calibration_mib:
+        copy_calibration(args.copy_calibration_mib)
     wl = WORKLOADS[args.workload]
     shape, k, B = wl.shape, wl.k_values[0], wl.batch
     plens = wl.prefix_lengths()
@@ -204,6 +250,7 @@ def main():
     dom = max((n for n in kernels), key=lambda n: kernels[n]["avg_us"] * kernels[n]["launches_per_step"])
     dom_avg_s = kernels[dom]["avg_us"] * 1e-6
     achieved = kb[dom] / dom_avg_s / 1e9
+    traffic = measured_traffic(dom) if args.workload == "8b" else None
     res = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -230,7 +277,7 @@ def main():
         "committed_tokens_per_s": round(committed / (elapsed_ms * 1e-3), 1),
         "device_status": status,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "bytes_per_launch": int(kb[dom]), "avg_launch_us": kernels[dom]["avg_us"]},
         "kernels": kernels,
     }

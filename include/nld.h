@@ -110,10 +110,13 @@ typedef struct {
  *   v: [n_layers][batch][n_kv_heads][max_len/64][head_dim][64]
  *      (64-position tiles, each stored transposed: head_dim rows of 64 positions)
  * lengths[b] = P_b, the committed length of sequence b.  Rows at positions
- * >= P_b are scratch: a block pass (either mode) writes its own K/V rows to
- * positions [P_b, P_b + k) and attends to them there, but only
+ * >= P_b are scratch: a verify pass writes its block's K/V rows to positions
+ * [P_b, P_b + k) (a draft pass writes no cache row), and only
  * nld_verify_accept advances lengths (by L+1), which commits the anchor row
- * and the accepted draft rows; the rest are overwritten by later passes. */
+ * and the accepted draft rows; the rest are overwritten by later passes.
+ * Within a pass the block attends to its own keys and values from a
+ * higher-precision copy in the workspace (bf16 value plus bf16 remainder),
+ * so the cache rows are only what a commit keeps. */
 typedef struct {
     void* k;
     void* v;
@@ -164,10 +167,10 @@ nld_status nld_workspace_init(void* workspace, size_t ws_bytes, void* stream);
 
 /* ---- the block-decode step ---------------------------------------------------
  * One forward pass over tokens[batch][k] (block row j at position P_b + j):
- * embedding -> n_layers x (RMSNorm, QKV, RoPE, K/V write to cache rows
- * [P_b, P_b+k), block-masked GQA attention over the P_b + k keys, O + residual,
- * RMSNorm, SwiGLU, down + residual) -> final RMSNorm -> LM head -> per-row
- * argmax (lowest index among equal maxima).
+ * embedding -> n_layers x (RMSNorm, QKV, RoPE, K/V write (verify: cache rows
+ * [P_b, P_b+k)), block-masked GQA attention over the P_b + k keys, O +
+ * residual, RMSNorm, SwiGLU, down + residual) -> final RMSNorm -> LM head ->
+ * per-row argmax (lowest index among equal maxima).
  * mode: NLD_MODE_VERIFY (block causal) or NLD_MODE_DRAFT (rows j >= bidir_from
  * see every block column, rows below it are causal); bidir_from in [0, k].
  * logits (optional) f32 [batch][k][vocab]; argmax (optional) int32 [batch][k].
@@ -181,8 +184,8 @@ nld_status nld_block_forward(const nld_model* m, const nld_kv_cache* kv, const i
 
 /* Diffusion draft (Sec. 3.3): runs the draft pass over [anchor[b], mask x (k-1)]
  * and writes draft[b][j-1] = argmax of draft row j, j = 1..k-1 (k >= 2).
- * logits optional as above.  Cache rows [P_b, P_b+k) are overwritten
- * (scratch); lengths unchanged.  Errors as nld_block_forward. */
+ * logits optional as above.  The cache is not written; lengths unchanged.
+ * Errors as nld_block_forward. */
 nld_status nld_draft(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor, int32_t batch, int32_t k,
                      int32_t bidir_from, int32_t* draft, float* logits, void* workspace, size_t ws_bytes,
                      void* stream);

@@ -294,6 +294,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.q_row_tiles = L.row_tiles;
         g.kc = kc;
         g.vc = vc;
+        g.write_cache = io.mode == NLD_MODE_VERIFY;
         g.blk_k = at<uint16_t>(ws, L.blk_k);
         g.blk_v = at<uint16_t>(ws, L.blk_v);
         g.lengths = kv->lengths;

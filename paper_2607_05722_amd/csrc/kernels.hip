@@ -87,8 +87,8 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
             store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out);
             continue;
         }
-        // K/V: bf16 into the cache (what a commit keeps), split into the block buffer
-        // (what this pass's attention over the block's own keys reads)
+        // K/V: split into the block buffer (what this pass's attention over the block's
+        // own keys reads) and, in a verify pass, bf16 into the cache (what a commit keeps)
         const int kvh = hh - nq - (kind == 2 ? nkv : 0);
         const size_t unit = (size_t)b * nkv + kvh;
         const uint16_t ob = (uint16_t)f32_to_bf16(out);
@@ -100,6 +100,7 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
             a.blk_v[(unit * 2 * D + dim) * 64 + jb] = ob;
             a.blk_v[((unit * 2 + 1) * D + dim) * 64 + jb] = lo;
         }
+        if (!a.write_cache) continue;
         if (pos >= a.max_len) atomicOr(a.status, DEV_CAPACITY);
         else if (kind == 1) a.kc[(unit * a.max_len + pos) * D + dim] = ob;
         else a.vc[((unit * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;

@@ -104,6 +104,7 @@ struct GemmArgs {
     int q_row_tiles;     // query-row tiles of 16 per (sequence, KV head)
     uint16_t* kc;        // this layer's K cache [batch][n_kv_heads][max_len][head_dim]
     uint16_t* vc;        // this layer's V cache [batch][n_kv_heads][max_len/64][head_dim][64]
+    int write_cache;     // verify: the block's K/V rows also go to cache rows [P_b, P_b + k)
     uint16_t* blk_k;     // the block's own keys, split: [unit][hi, lo][64 rows][head_dim]
     uint16_t* blk_v;     // the block's own values, split: [unit][hi, lo][head_dim][64 rows]
     const int32_t* lengths;

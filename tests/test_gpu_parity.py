@@ -271,6 +271,7 @@ def test_8b_layer_block_pass(R, layer8b, k, mode):
     tok = synth_tokens(shape, t["seed"], "8b_layer.block%d" % k, (1, k))
     ref, nk, nv = O.block_forward(t["w"], t["okv"], tok, mode)
     ws = R.Workspace(t["model"], 1, k, t["cache"].max_len)
+    before = t["cache"].read_kv(0, 2048, 2048 + k)
     logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(tok).cuda(),
                                  R.VERIFY if mode == O.VERIFY else R.DRAFT)
     g = logits.cpu().numpy()
@@ -279,6 +280,9 @@ def test_8b_layer_block_pass(R, layer8b, k, mode):
     assert e <= TOL
     check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
     kg, vg = t["cache"].read_kv(0, 2048, 2048 + k)
-    assert rel_err(O.bf16_bits_to_float(kg), nk[0]) < TOL
-    assert rel_err(O.bf16_bits_to_float(vg), nv[0]) < TOL
+    if mode == O.VERIFY:     # the verify pass leaves its K/V rows in the uncommitted cache rows
+        assert rel_err(O.bf16_bits_to_float(kg), nk[0]) < TOL
+        assert rel_err(O.bf16_bits_to_float(vg), nv[0]) < TOL
+    else:                    # a draft pass writes no cache row
+        assert np.array_equal(kg, before[0]) and np.array_equal(vg, before[1])
     assert R.read_device_status(ws) == 0
