@@ -576,12 +576,9 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const bool row_ok = computes && row < R;
     const int j = row_ok ? row % k : 0;
 
-    int P = a.lengths[b];
-    P = P < 0 ? 0 : (P > a.max_len ? a.max_len : P);
-    // prefix splits cover committed keys [kbeg, kend) of [0, P); the block part covers [P, P + k)
-    const int kbeg = blockpart ? P : split * a.chunk;
-    const int kend = blockpart ? P + k : min(kbeg + a.chunk, P);
+    const int P_raw = a.lengths[b];   // requested first; the loads below do not depend on it
     const bool bidir_row = (a.mode == 1) && (j >= a.bidir_from);
+    const int split_beg = split * a.chunk;   // prefix splits: first key of the split (< max_len)
 
     const size_t head_off = (size_t)(b * nkv + kvh) * a.max_len * D;
     const uint16_t* kbase = a.kc + head_off;   // where gload reads stages from
@@ -648,6 +645,31 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
             qb[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 1024) : zero4;
             ql[c] = row_ok ? *(const uint4*)(qp + (size_t)c * 1024 + SPLIT_LO) : zero4;
         }
+    }
+    // The first stage is requested before the committed length is known: a prefix split's
+    // first 64 keys (always inside the cache; masked below if they are not committed), or
+    // the block part's hi and lo halves.
+    Stage s0{}, s1{}, s2{};
+    if (blockpart) {
+        const size_t kv_unit = (size_t)unit * 2 * 64 * D;
+        kbase = a.blk_k + kv_unit;
+        vbase = a.blk_v + kv_unit;
+        s0 = gload(0);
+        kbase += 64 * D;
+        vbase += 64 * D;
+        s1 = gload(0);
+    } else {
+        s0 = gload(split_beg);
+    }
+
+    int P = P_raw < 0 ? 0 : (P_raw > a.max_len ? a.max_len : P_raw);
+    // prefix splits cover committed keys [kbeg, kend) of [0, P); the block part covers [P, P + k)
+    const int kbeg = blockpart ? P : split_beg;
+    const int kend = blockpart ? P + k : min(kbeg + a.chunk, P);
+    const int nst = blockpart ? 1 : (kend > kbeg ? (kend - kbeg + 63) / 64 : 0);
+    if (!blockpart) {
+        if (nst > 1) s1 = gload(kbeg + 64);
+        if (nst > 2) s2 = gload(kbeg + 128);
     }
 
     f32x4_t acc[DT];
@@ -737,32 +759,27 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     };
 
     if (blockpart) {
-        // one stage (k <= 64): hi halves into slot 0, lo halves into slot 1
-        const size_t kv_unit = (size_t)unit * 2 * 64 * D;
-        kbase = a.blk_k + kv_unit;
-        vbase = a.blk_v + kv_unit;
-        lstore(gload(0), 0);
-        kbase += 64 * D;
-        vbase += 64 * D;
-        lstore(gload(0), 1);
+        // one stage (k <= 64): hi halves in slot 0, lo halves in slot 1
+        lstore(s0, 0);
+        lstore(s1, 1);
         __syncthreads();
         compute(kbeg, 0, true);
         __syncthreads();
     } else {
-        // stages of 64 keys; two stages in flight in registers while one is multiplied from LDS
-        const int nst = kend > kbeg ? (kend - kbeg + 63) / 64 : 0;
-        Stage n1{}, n2{};
-        if (nst > 0) {
-            lstore(gload(kbeg), 0);
-            if (nst > 1) n1 = gload(kbeg + 64);
-            if (nst > 2) n2 = gload(kbeg + 128);
-        }
+        // Stages of 64 keys.  Stage st is multiplied from LDS slot st & 1 while stages st+1
+        // and st+2 are in flight in registers (s1 and s2 by turns; the loop is unrolled by
+        // two so that no register copy waits on a load still in flight).
+        if (nst > 0) lstore(s0, 0);
         __syncthreads();
-        for (int st = 0; st < nst; ++st) {
-            compute(kbeg + 64 * st, st & 1, false);
-            if (st + 1 < nst) lstore(n1, (st + 1) & 1);
-            n1 = n2;
-            if (st + 3 < nst) n2 = gload(kbeg + 64 * (st + 3));
+        for (int st = 0; st < nst; st += 2) {
+            compute(kbeg + 64 * st, 0, false);
+            if (st + 1 < nst) lstore(s1, 1);
+            if (st + 3 < nst) s1 = gload(kbeg + 64 * (st + 3));
+            __syncthreads();
+            if (st + 1 >= nst) break;
+            compute(kbeg + 64 * (st + 1), 1, false);
+            if (st + 2 < nst) lstore(s2, 0);
+            if (st + 4 < nst) s2 = gload(kbeg + 64 * (st + 4));
             __syncthreads();
         }
     }
