@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, po, pml, blk_k, blk_v, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, rope, po, pml, blk_k, blk_v, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -119,6 +119,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.o = take(4 * L.Mpad * QD);
     L.act = take(4 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
+    L.rope = take(8 * L.Mpad * (size_t)(c.head_dim / 2));
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
     L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
@@ -272,6 +273,11 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.xg = at<uint16_t>(ws, L.xg);
     e.part_ss = at<float>(ws, L.part_ss);
     e.status = status;
+    e.rope = at<float2>(ws, L.rope);
+    e.lengths = kv->lengths;
+    e.max_len = kv->max_len;
+    e.head_dim = c.head_dim;
+    for (int i = 0; i < c.head_dim / 2; ++i) e.inv_freq[i] = pow((double)c.rope_base, -2.0 * i / (double)c.head_dim);
     {
         TraceScope ts(NLD_TRACE_EMBED, s);
         HIP_TRY(launch_embed(e, s));
@@ -303,7 +309,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.n_kv_heads = nkv;
         g.head_dim = D;
         g.max_len = kv->max_len;
-        for (int i = 0; i < D / 2; ++i) g.inv_freq[i] = pow((double)c.rope_base, -2.0 * i / (double)D);
+        g.rope = at<float2>(ws, L.rope);
         g.status = status;
         {
             TraceScope ts(NLD_TRACE_QKV, s);

@@ -46,14 +46,15 @@ __device__ __forceinline__ float wave_sum(float v) {
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) { return a > b ? a : b; }
 
 // =====================================================================================
-// GEMM epilogues.  v holds C[4g+i][r] of a 16x16 output tile (rows mbase..+16, packed
-// column tile t); lane = 16g + r.  inv(i) is the RMSNorm scale of row mbase+4g+i.
+// GEMM epilogues, one output row per call.  A 16x16 output tile (packed column tile
+// t) is finished by up to four wavefronts together: the wavefront that takes index i
+// handles rows 4g + i of the tile (g = lane / 16) and lane 16g + r holds column r.
+// y is the finished (RMSNorm-scaled) value of row m, column r.
 // =====================================================================================
-// pos(i): absolute position of row mbase+4g+i (block row j at P_b + j).
-template <typename InvFn, typename PosFn>
-__device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, InvFn inv,
-                                        PosFn pos_of) {
-    const int r = lane & 15, g = lane >> 4;
+// pos: absolute position of row m (block row j at P_b + j).  RoPE uses the per-row
+// (cos, sin) table built by the embedding kernel.
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, float y, int m, int t, int lane, int pos) {
+    const int r = lane & 15;
     const int D = a.head_dim;
     const int tiles_per_head = D / 16;
     const int hh = t / tiles_per_head, u = t % tiles_per_head;
@@ -61,113 +62,81 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, f32x4_t v, int mbase,
     const int dim = (r < 8) ? fi : D / 2 + fi;  // lanes r and r^8 hold the pair (fi, fi + D/2)
     const int nq = a.n_q_heads, nkv = a.n_kv_heads;
     const int kind = hh < nq ? 0 : (hh < nq + nkv ? 1 : 2);
-    const double inv_freq = a.inv_freq[fi];
-    const double two_pi = 6.283185307179586476925286766559;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = mbase + 4 * g + i;
-        const bool ok = m < a.M;
-        const float y = v[i] * inv(i);
-        const float partner = __shfl_xor(y, 8);
-        const int pos = pos_of(i);
-        float out = y;
-        if (kind < 2) {
-            // angle pos * base^(-2 fi / D) reduced to [-pi, pi] in fp64, then sin/cos in fp32
-            double ang = (double)pos * inv_freq;
-            ang -= two_pi * rint(ang * (1.0 / two_pi));
-            const float af = (float)ang;
-            const float sn = __sinf(af), cs = __cosf(af);
-            out = (r < 8) ? (y * cs - partner * sn) : (y * cs + partner * sn);
-        }
-        if (!ok) continue;
-        const int b = m / a.k_blk, jb = m - b * a.k_blk;
-        if (kind == 0) {
-            const int G = nq / nkv;
-            const int row = (hh % G) * a.k_blk + jb;
-            store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out);
-            continue;
-        }
-        // K/V: split into the block buffer (what this pass's attention over the block's
-        // own keys reads) and, in a verify pass, bf16 into the cache (what a commit keeps)
-        const int kvh = hh - nq - (kind == 2 ? nkv : 0);
-        const size_t unit = (size_t)b * nkv + kvh;
-        const uint16_t ob = (uint16_t)f32_to_bf16(out);
-        const uint16_t lo = (uint16_t)f32_to_bf16(out - bf16_to_f32(ob));
-        if (kind == 1) {
-            a.blk_k[(unit * 2 * 64 + jb) * D + dim] = ob;
-            a.blk_k[((unit * 2 + 1) * 64 + jb) * D + dim] = lo;
-        } else {
-            a.blk_v[(unit * 2 * D + dim) * 64 + jb] = ob;
-            a.blk_v[((unit * 2 + 1) * D + dim) * 64 + jb] = lo;
-        }
-        if (!a.write_cache) continue;
-        if (pos >= a.max_len) atomicOr(a.status, DEV_CAPACITY);
-        else if (kind == 1) a.kc[(unit * a.max_len + pos) * D + dim] = ob;
-        else a.vc[((unit * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;
+    const bool ok = m < a.M;
+    const float partner = __shfl_xor(y, 8);
+    float out = y;
+    if (kind < 2) {
+        const float2 cs = a.rope[(size_t)(ok ? m : 0) * (D / 2) + fi];
+        out = (r < 8) ? (y * cs.x - partner * cs.y) : (y * cs.x + partner * cs.y);
     }
+    if (!ok) return;
+    const int b = m / a.k_blk, jb = m - b * a.k_blk;
+    if (kind == 0) {
+        const int G = nq / nkv;
+        const int row = (hh % G) * a.k_blk + jb;
+        store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out);
+        return;
+    }
+    // K/V: split into the block buffer (what this pass's attention over the block's
+    // own keys reads) and, in a verify pass, bf16 into the cache (what a commit keeps)
+    const int kvh = hh - nq - (kind == 2 ? nkv : 0);
+    const size_t unit = (size_t)b * nkv + kvh;
+    const uint16_t ob = (uint16_t)f32_to_bf16(out);
+    const uint16_t lo = (uint16_t)f32_to_bf16(out - bf16_to_f32(ob));
+    if (kind == 1) {
+        a.blk_k[(unit * 2 * 64 + jb) * D + dim] = ob;
+        a.blk_k[((unit * 2 + 1) * 64 + jb) * D + dim] = lo;
+    } else {
+        a.blk_v[(unit * 2 * D + dim) * 64 + jb] = ob;
+        a.blk_v[((unit * 2 + 1) * D + dim) * 64 + jb] = lo;
+    }
+    if (!a.write_cache) return;
+    if (pos >= a.max_len) atomicOr(a.status, DEV_CAPACITY);
+    else if (kind == 1) a.kc[(unit * a.max_len + pos) * D + dim] = ob;
+    else a.vc[((unit * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;
 }
 
-template <typename InvFn>
-__device__ __forceinline__ void epi_swiglu(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, InvFn inv) {
-    const int r = lane & 15, g = lane >> 4;
+__device__ __forceinline__ void epi_swiglu(const GemmArgs& a, float y, int m, int t, int lane) {
+    const int r = lane & 15;
     const int col = 8 * t + (r & 7);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = mbase + 4 * g + i;
-        const float y = v[i] * inv(i);
-        const float partner = __shfl_xor(y, 8);   // lanes r < 8 hold gate columns, r^8 the matching up columns
-        if (m < a.M && r < 8 && col < a.ffn) {
-            const float gate = y, up = partner;
-            const float act = gate / (1.0f + expf(-gate)) * up;
-            store_split(a.act, split_index(m, col, (a.ffn + 31) / 32), act);
-        }
+    const float partner = __shfl_xor(y, 8);   // lanes r < 8 hold gate columns, r^8 the matching up columns
+    if (m < a.M && r < 8 && col < a.ffn) {
+        const float act = y / (1.0f + expf(-y)) * partner;
+        store_split(a.act, split_index(m, col, (a.ffn + 31) / 32), act);
     }
 }
 
-// Returns, in every lane with r == 0, the argmax keys of rows mbase+4g+i over this tile.
-template <typename InvFn>
-__device__ __forceinline__ void epi_lmhead(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, InvFn inv,
-                                           unsigned long long (&key_run)[4]) {
-    const int r = lane & 15, g = lane >> 4;
+// Returns, in every lane, the argmax key of row m over this tile's 16 columns.
+__device__ __forceinline__ unsigned long long epi_lmhead(const GemmArgs& a, float y, int m, int t, int lane) {
+    const int r = lane & 15;
     const int n = t * 16 + r;
-    const bool col_ok = n < a.vocab;
+    const bool ok = m < a.M && n < a.vocab;
+    if (ok && a.logits) a.logits[(size_t)m * a.vocab + n] = y;
+    unsigned long long key = ok ? argmax_key(y, (uint32_t)n) : 0ull;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = mbase + 4 * g + i;
-        const bool ok = m < a.M;
-        const float y = v[i] * inv(i);
-        if (ok && col_ok && a.logits) a.logits[(size_t)m * a.vocab + n] = y;
-        unsigned long long key = (ok && col_ok) ? argmax_key(y, (uint32_t)n) : 0ull;
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) key = umax64(key, __shfl_xor(key, off));
-        key_run[i] = umax64(key_run[i], key);
-    }
+    for (int off = 1; off < 16; off <<= 1) key = umax64(key, __shfl_xor(key, off));
+    return key;
 }
 
-// xres[i]: the residual x[mbase+4g+i][16t+r], loaded when the workgroup started.
-// Writes x += v, the next RMSNorm's bf16 operand x * gain_next and, per row, the
-// sum of x^2 over the tile's 16 columns.
-__device__ __forceinline__ void epi_resid(const GemmArgs& a, f32x4_t v, int mbase, int t, int lane, const float (&xres)[4]) {
-    const int r = lane & 15, g = lane >> 4;
+// xres: the residual x[m][16t + r].  Writes x += v, the next RMSNorm's split operand
+// x * gain_next and the row's sum of x^2 over the tile's 16 columns.
+__device__ __forceinline__ void epi_resid(const GemmArgs& a, float v, int m, int t, int lane, float xres) {
+    const int r = lane & 15;
     const int N = a.n_tiles * 16;
     const int n = t * 16 + r;
     const float gn = bf16_to_f32(a.gain_next[n]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = mbase + 4 * g + i;
-        const bool ok = m < a.M;
-        const float xn = xres[i] + v[i];
-        if (ok) {
-            a.x[(size_t)m * N + n] = xn;
-            store_split(a.xg_out, split_index(m, n, N / 32), xn * gn);
-        }
-        float sq = ok ? xn * xn : 0.f;
-        sq += __shfl_xor(sq, 1);
-        sq += __shfl_xor(sq, 2);
-        sq += __shfl_xor(sq, 4);
-        sq += __shfl_xor(sq, 8);
-        if (r == 0 && ok) a.part_ss_out[(size_t)m * a.n_tiles + t] = sq;
+    const bool ok = m < a.M;
+    const float xn = xres + v;
+    if (ok) {
+        a.x[(size_t)m * N + n] = xn;
+        store_split(a.xg_out, split_index(m, n, N / 32), xn * gn);
     }
+    float sq = ok ? xn * xn : 0.f;
+    sq += __shfl_xor(sq, 1);
+    sq += __shfl_xor(sq, 2);
+    sq += __shfl_xor(sq, 4);
+    sq += __shfl_xor(sq, 8);
+    if (r == 0 && ok) a.part_ss_out[(size_t)m * a.n_tiles + t] = sq;
 }
 
 // 1/rms for `rows` rows starting at m0 from the producer's 16-column partial sums
@@ -206,6 +175,9 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     __shared__ int pos_s[16];
 
     const int NW = blockDim.x >> 6;
+    if constexpr (EPI == EPI_LMHEAD) {
+        if (threadIdx.x < 256) key_s[threadIdx.x >> 4][threadIdx.x & 15] = 0ull;
+    }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int T = a.n_tiles, G = gridDim.x;
@@ -237,10 +209,10 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
         }
     }
     __syncthreads();
-    auto inv = [&](int i) { return inv_s[4 * g + i]; };
-    auto pos_of = [&](int i) { return pos_s[4 * g + i]; };
 
-    unsigned long long key_run[4] = {0ull, 0ull, 0ull, 0ull};
+    // A tile is finished by FIN wavefronts (wavefront i of the group takes rows 4g + i,
+    // 4g + i + FIN, ...); the groups take the tiles in turn.
+    const int FIN = NW < 4 ? NW : 4, groups = NW / FIN;
     for (int t = tb; t < te; ++t) {
         f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, accl = {0.f, 0.f, 0.f, 0.f};
         const bool more = t + 1 < te;
@@ -254,21 +226,25 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
         const int parity = (t - tb) & 1;
         red[parity][wave][lane] = acc + accl;
         __syncthreads();
-        if (wave == (t - tb) % NW) {
-            f32x4_t v = red[parity][0][lane];
-            for (int w = 1; w < NW; ++w) v += red[parity][w][lane];
-            if constexpr (EPI == EPI_QKV) epi_qkv(a, v, 0, t, lane, inv, pos_of);
-            else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, 0, t, lane, inv);
-            else epi_lmhead(a, v, 0, t, lane, inv, key_run);
+        if (wave / FIN == (t - tb) % groups) {
+            const float* rp = (const float*)&red[parity][0][lane];
+            for (int i = wave % FIN; i < 4; i += FIN) {
+                float v = rp[i];
+                for (int w = 1; w < NW; ++w) v += rp[w * 256 + i];   // fixed order over the K-slices
+                const int m = 4 * g + i;
+                const float y = v * inv_s[m];
+                if constexpr (EPI == EPI_QKV) epi_qkv(a, y, m, t, lane, pos_s[m]);
+                else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, y, m, t, lane);
+                else {
+                    const unsigned long long key = epi_lmhead(a, y, m, t, lane);
+                    if (r == 0) key_s[wave][m] = umax64(key_s[wave][m], key);
+                }
+            }
         }
     }
 
     if constexpr (EPI == EPI_LMHEAD) {
         // one argmax key per row for this workgroup
-        if (r == 0) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) key_s[wave][4 * g + i] = key_run[i];
-        }
         __syncthreads();
         if ((int)threadIdx.x < a.M && threadIdx.x < 16) {
             unsigned long long best = 0ull;
@@ -368,17 +344,18 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
             for (int ct = 0; ct < CT; ++ct) accl[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    // residual values for the epilogue of this wavefront's first tile, fetched up front
-    float xres[4] = {0.f, 0.f, 0.f, 0.f};
+    // Epilogue assignment: a tile is finished by FIN = 4 wavefronts, wavefront i of the
+    // group taking rows 4g + i; the NW / 4 groups take the MT x CT tiles in turn.
+    constexpr int FIN = 4, GROUPS = NW / FIN;
+    static_assert(NW % FIN == 0, "wavefront count must be a multiple of 4");
+    const int fi_row = wave % FIN, ti0 = wave / FIN;
+    // residual value for this wavefront's first epilogue row, fetched up front
+    float xres0 = 0.f;
     if constexpr (EPI == EPI_RESID) {
-        if (wave < MT * CT) {
-            const int mt = wave / CT, ct = wave % CT;
-            const int n = (t0 + ct) * 16 + r;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int m = m0 + 16 * mt + 4 * g + i;
-                if (m < a.M && t0 + ct < a.n_tiles) xres[i] = a.x[(size_t)m * a.n_tiles * 16 + n];
-            }
+        if (ti0 < MT * CT) {
+            const int mt = ti0 / CT, ct = ti0 % CT;
+            const int m = m0 + 16 * mt + 4 * g + fi_row;
+            if (m < a.M && t0 + ct < a.n_tiles) xres0 = a.x[(size_t)m * a.n_tiles * 16 + (t0 + ct) * 16 + r];
         }
     }
 
@@ -435,38 +412,29 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         if (threadIdx.x < 16 * MT) key_s[threadIdx.x] = 0ull;
     }
     __syncthreads();
-    for (int ti = wave; ti < MT * CT; ti += NW) {
-        f32x4_t v = red[0][ti][lane];
+    for (int ti = ti0; ti < MT * CT; ti += GROUPS) {
+        const float* rp = (const float*)&red[0][ti][lane];
+        float v = rp[fi_row];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) v += red[w][ti][lane];
+        for (int w = 1; w < NW; ++w) v += rp[w * MT * CT * 256 + fi_row];   // fixed order over the K-slices
         const int mt = ti / CT, ct = ti % CT;
         const int t = t0 + ct;
         if (t >= a.n_tiles) continue;
-        const int mbase = m0 + 16 * mt;
-        auto inv = [&](int i) { return inv_s[16 * mt + 4 * g + i]; };
-        auto pos_of = [&](int i) {
-            const int m = min(mbase + 4 * g + i, a.M - 1);
-            return committed_length(a.lengths, m / a.k_blk, a.max_len, a.status) + m % a.k_blk;
-        };
+        const int ml = 16 * mt + 4 * g + fi_row;   // row within the workgroup's rows
+        const int m = m0 + ml;
         if constexpr (EPI == EPI_RESID) {
-            if (ti != wave) {   // only when a wavefront finishes more than one tile
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int m = mbase + 4 * g + i;
-                    xres[i] = m < a.M ? a.x[(size_t)m * a.n_tiles * 16 + t * 16 + r] : 0.f;
-                }
-            }
-            epi_resid(a, v, mbase, t, lane, xres);
-        }
-        else if constexpr (EPI == EPI_QKV) epi_qkv(a, v, mbase, t, lane, inv, pos_of);
-        else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, v, mbase, t, lane, inv);
-        else {
-            unsigned long long kr[4] = {0ull, 0ull, 0ull, 0ull};
-            epi_lmhead(a, v, mbase, t, lane, inv, kr);
-            if (r == 0) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) atomicMax(&key_s[16 * mt + 4 * g + i], kr[i]);
-            }
+            float xr = xres0;
+            if (ti != ti0) xr = m < a.M ? a.x[(size_t)m * a.n_tiles * 16 + t * 16 + r] : 0.f;
+            epi_resid(a, v, m, t, lane, xr);
+        } else if constexpr (EPI == EPI_QKV) {
+            const int mc = min(m, a.M - 1);
+            const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
+            epi_qkv(a, v * inv_s[ml], m, t, lane, pos);
+        } else if constexpr (EPI == EPI_SWIGLU) {
+            epi_swiglu(a, v * inv_s[ml], m, t, lane);
+        } else {
+            const unsigned long long key = epi_lmhead(a, v * inv_s[ml], m, t, lane);
+            if (r == 0) atomicMax(&key_s[ml], key);
         }
     }
     if constexpr (EPI == EPI_LMHEAD) {
@@ -905,6 +873,16 @@ hipError_t launch_attention_combine(int head_dim, int units, int rows, const Att
 __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
     const int m = blockIdx.x;
     const int b = m / a.k_blk, j = m % a.k_blk;
+    // RoPE table of this row (used by every layer's QKV epilogue): angle pos * theta_i
+    // reduced to [-pi, pi] and evaluated in fp64, stored as fp32 (cos, sin).
+    if ((int)threadIdx.x < a.head_dim / 2) {
+        const int fi = threadIdx.x;
+        const int pos = committed_length(a.lengths, b, a.max_len, a.status) + j;
+        const double two_pi = 6.283185307179586476925286766559;
+        double ang = (double)pos * a.inv_freq[fi];
+        ang -= two_pi * rint(ang * (1.0 / two_pi));
+        a.rope[(size_t)m * (a.head_dim / 2) + fi] = float2{(float)cos(ang), (float)sin(ang)};
+    }
     int tok;
     if (a.source == 0) tok = a.tokens[m];
     else if (j == 0) tok = a.anchor[b];

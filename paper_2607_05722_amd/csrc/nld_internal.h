@@ -110,7 +110,7 @@ struct GemmArgs {
     const int32_t* lengths;
     int k_blk;
     int n_q_heads, n_kv_heads, head_dim, max_len;
-    double inv_freq[64];  // RoPE frequencies base^(-2i/head_dim), i < head_dim/2 (computed on the host in fp64)
+    const float2* rope;  // [M][head_dim/2] (cos, sin) of each row's RoPE angles (embedding kernel)
     uint32_t* status;
     // EPI_SWIGLU
     uint16_t* act;       // split bf16 silu(gate) * up, split_index with ceil(ffn/32) steps
@@ -158,6 +158,11 @@ struct EmbedArgs {
     uint16_t* xg;           // split x * gain, split_index with hidden/32 steps
     float* part_ss;         // [M][hidden/16]
     uint32_t* status;
+    // RoPE table: rope[m][i] = (cos, sin) of (P_b + j) * inv_freq[i], i < head_dim/2
+    float2* rope;
+    const int32_t* lengths;
+    int max_len, head_dim;
+    double inv_freq[64];    // base^(-2i/head_dim), computed on the host in fp64
 };
 
 enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2 };
