@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, rope, po, pml, blk_k, blk_v, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, rope, po, pml, blk_k, blk_v, tile_ctr, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -120,6 +120,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.act = take(4 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
     L.rope = take(8 * L.Mpad * (size_t)(c.head_dim / 2));
+    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1));   // per pass: QKV and gate/up of every layer, LM head
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
     L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
@@ -163,11 +164,13 @@ bool plan_norm(int epi, int M, int ksteps, int* ks, int* waves) {
     return false;
 }
 
-// Workgroups for n_tiles tiles: about one per CU, balanced contiguous ranges.
+// Workgroups of the normed GEMM: one per CU, but at least two tiles per workgroup on
+// average (each workgroup loads the whole operand once); tiles beyond the first one per
+// workgroup are handed out dynamically.
 int norm_grid(int n_tiles) {
     const int cus = env_int("NLD_CUS", 256);
-    const int per = cdiv(n_tiles, cus);
-    return cdiv(n_tiles, per);
+    const int half = (n_tiles + 1) / 2;
+    return half < cus ? half : cus;
 }
 
 struct StreamPlan {
@@ -274,6 +277,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.part_ss = at<float>(ws, L.part_ss);
     e.status = status;
     e.rope = at<float2>(ws, L.rope);
+    e.tile_ctr = at<unsigned>(ws, L.tile_ctr);
+    e.n_tile_ctr = 2 * c.n_layers + 1;
     e.lengths = kv->lengths;
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;
@@ -310,6 +315,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.head_dim = D;
         g.max_len = kv->max_len;
         g.rope = at<float2>(ws, L.rope);
+        g.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * l;
         g.status = status;
         {
             TraceScope ts(NLD_TRACE_QKV, s);
@@ -370,6 +376,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gu.ksteps = ks_h;
         gu.act = at<uint16_t>(ws, L.act);
         gu.ffn = c.ffn;
+        gu.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * l + 1;
         {
             TraceScope ts(NLD_TRACE_GATE_UP, s);
             HIP_TRY(normed_gemm(EPI_SWIGLU, gu, ws, L, s, nullptr));
@@ -394,6 +401,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     }
 
     GemmArgs gl{};
+    gl.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * c.n_layers;
     gl.eps = c.rms_eps;
     gl.M = M;
     gl.K = c.hidden;

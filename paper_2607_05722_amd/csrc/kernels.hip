@@ -174,6 +174,8 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     __shared__ unsigned long long key_s[16][16];
     __shared__ int pos_s[16];
 
+    __shared__ int next_s[2];
+
     const int NW = blockDim.x >> 6;
     if constexpr (EPI == EPI_LMHEAD) {
         if (threadIdx.x < 256) key_s[threadIdx.x >> 4][threadIdx.x & 15] = 0ull;
@@ -181,13 +183,19 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int T = a.n_tiles, G = gridDim.x;
-    const int tb = (int)((long long)T * blockIdx.x / G);
-    const int te = (int)((long long)T * (blockIdx.x + 1) / G);
     const int s0 = wave * KS;
 
+    // Tiles are handed out dynamically: workgroup b starts with tile b, further tiles
+    // come from a counter (tile index G + counter), requested one tile ahead so that
+    // the atomic's latency hides behind the current tile.  Faster workgroups (and
+    // XCDs) end up with more tiles.
+    int cur = blockIdx.x;
+    unsigned grab = 0u;
+    if (threadIdx.x == 0 && G < T) grab = atomicAdd(a.tile_ctr, 1u);
+
     uint4 wb[KS];
-    if (tb < te) {
-        const uint4* p = a.W + ((size_t)tb * a.ksteps + s0) * 64 + lane;
+    if (cur < T) {
+        const uint4* p = a.W + ((size_t)cur * a.ksteps + s0) * 64 + lane;
 #pragma unroll
         for (int s = 0; s < KS; ++s) wb[s] = p[(size_t)s * 64];
     }
@@ -208,25 +216,31 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
             pos_s[threadIdx.x] = committed_length(a.lengths, m / a.k_blk, a.max_len, a.status) + m % a.k_blk;
         }
     }
+    if (threadIdx.x == 0) next_s[0] = G < T ? min(G + (int)grab, T) : T;
     __syncthreads();
 
     // A tile is finished by FIN wavefronts (wavefront i of the group takes rows 4g + i,
     // 4g + i + FIN, ...); the groups take the tiles in turn.
     const int FIN = NW < 4 ? NW : 4, groups = NW / FIN;
-    for (int t = tb; t < te; ++t) {
+    for (int it = 0; cur < T; ++it) {
+        const int t = cur;
+        const int nxt = next_s[it & 1];   // its weights stream in while tile t is multiplied
+        if (threadIdx.x == 0 && nxt < T) grab = atomicAdd(a.tile_ctr, 1u);
         f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, accl = {0.f, 0.f, 0.f, 0.f};
-        const bool more = t + 1 < te;
-        const uint4* p = a.W + ((size_t)(t + 1) * a.ksteps + s0) * 64 + lane;
+        const bool more = nxt < T;
+        const uint4* p = a.W + ((size_t)nxt * a.ksteps + s0) * 64 + lane;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             acc = mfma_16x16x32(ah[s], wb[s], acc);
             accl = mfma_16x16x32(al[s], wb[s], accl);
             if (more) wb[s] = p[(size_t)s * 64];
         }
-        const int parity = (t - tb) & 1;
+        if (threadIdx.x == 0) next_s[(it + 1) & 1] = nxt < T ? min(G + (int)grab, T) : T;
+        const int parity = it & 1;
         red[parity][wave][lane] = acc + accl;
         __syncthreads();
-        if (wave / FIN == (t - tb) % groups) {
+        cur = nxt;
+        if (wave / FIN == it % groups) {
             const float* rp = (const float*)&red[parity][0][lane];
             for (int i = wave % FIN; i < 4; i += FIN) {
                 float v = rp[i];
@@ -873,6 +887,8 @@ hipError_t launch_attention_combine(int head_dim, int units, int rows, const Att
 __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
     const int m = blockIdx.x;
     const int b = m / a.k_blk, j = m % a.k_blk;
+    if (m == 0)
+        for (int i = threadIdx.x; i < a.n_tile_ctr; i += blockDim.x) a.tile_ctr[i] = 0u;
     // RoPE table of this row (used by every layer's QKV epilogue): angle pos * theta_i
     // reduced to [-pi, pi] and evaluated in fp64, stored as fp32 (cos, sin).
     if ((int)threadIdx.x < a.head_dim / 2) {

@@ -94,6 +94,7 @@ struct GemmArgs {
     const uint4* W;      // packed weights: [n_tiles][ksteps][64 lanes] x 16 bytes
     int n_tiles;
     int ksteps;          // ceil(K / 32)
+    unsigned* tile_ctr;  // normed GEMM: dynamic tile counter (zeroed by the embedding kernel each pass)
     // EPI_RESID: x += A W^T, then the next RMSNorm's operand and statistics
     float* x;
     uint16_t* xg_out;          // split x * gain_next, split_index with N/32 steps
@@ -158,6 +159,8 @@ struct EmbedArgs {
     uint16_t* xg;           // split x * gain, split_index with hidden/32 steps
     float* part_ss;         // [M][hidden/16]
     uint32_t* status;
+    unsigned* tile_ctr;     // [n_tile_ctr] dynamic tile counters of this pass's GEMMs, zeroed here
+    int n_tile_ctr;
     // RoPE table: rope[m][i] = (cos, sin) of (P_b + j) * inv_freq[i], i < head_dim/2
     float2* rope;
     const int32_t* lengths;
