@@ -118,13 +118,13 @@ __device__ __forceinline__ unsigned long long epi_lmhead(const GemmArgs& a, floa
     return key;
 }
 
-// xres: the residual x[m][16t + r].  Writes x += v, the next RMSNorm's split operand
-// x * gain_next and the row's sum of x^2 over the tile's 16 columns.
-__device__ __forceinline__ void epi_resid(const GemmArgs& a, float v, int m, int t, int lane, float xres) {
+// xres: the residual x[m][16t + r]; gn: the next RMSNorm's gain at column 16t + r.
+// Writes x += v, the next RMSNorm's split operand x * gain_next and the row's sum of
+// x^2 over the tile's 16 columns.
+__device__ __forceinline__ void epi_resid(const GemmArgs& a, float v, int m, int t, int lane, float xres, float gn) {
     const int r = lane & 15;
     const int N = a.n_tiles * 16;
     const int n = t * 16 + r;
-    const float gn = bf16_to_f32(a.gain_next[n]);
     const bool ok = m < a.M;
     const float xn = xres + v;
     if (ok) {
@@ -363,13 +363,17 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     constexpr int FIN = 4, GROUPS = NW / FIN;
     static_assert(NW % FIN == 0, "wavefront count must be a multiple of 4");
     const int fi_row = wave % FIN, ti0 = wave / FIN;
-    // residual value for this wavefront's first epilogue row, fetched up front
-    float xres0 = 0.f;
+    // residual value and next gain for this wavefront's first epilogue row, fetched up
+    // front so that the epilogue waits on no load
+    float xres0 = 0.f, gn0 = 0.f;
     if constexpr (EPI == EPI_RESID) {
         if (ti0 < MT * CT) {
             const int mt = ti0 / CT, ct = ti0 % CT;
             const int m = m0 + 16 * mt + 4 * g + fi_row;
-            if (m < a.M && t0 + ct < a.n_tiles) xres0 = a.x[(size_t)m * a.n_tiles * 16 + (t0 + ct) * 16 + r];
+            if (t0 + ct < a.n_tiles) {
+                gn0 = bf16_to_f32(a.gain_next[(t0 + ct) * 16 + r]);
+                if (m < a.M) xres0 = a.x[(size_t)m * a.n_tiles * 16 + (t0 + ct) * 16 + r];
+            }
         }
     }
 
@@ -437,9 +441,12 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         const int ml = 16 * mt + 4 * g + fi_row;   // row within the workgroup's rows
         const int m = m0 + ml;
         if constexpr (EPI == EPI_RESID) {
-            float xr = xres0;
-            if (ti != ti0) xr = m < a.M ? a.x[(size_t)m * a.n_tiles * 16 + t * 16 + r] : 0.f;
-            epi_resid(a, v, m, t, lane, xr);
+            float xr = xres0, gn = gn0;
+            if (ti != ti0) {
+                xr = m < a.M ? a.x[(size_t)m * a.n_tiles * 16 + t * 16 + r] : 0.f;
+                gn = bf16_to_f32(a.gain_next[t * 16 + r]);
+            }
+            epi_resid(a, v, m, t, lane, xr, gn);
         } else if constexpr (EPI == EPI_QKV) {
             const int mc = min(m, a.M - 1);
             const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
