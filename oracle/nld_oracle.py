@@ -19,6 +19,10 @@ What it computes (arXiv 2607.05722):
 * Mode 1 (Sec. 3.1), AR decoding, is the verify pass with a one-token block.
 * The first-mismatch index j* of the LoRA paragraph in Sec. 3.3 restates the
   acceptance rule and is the form used here.
+* Mode 2 (Sec. 3.2), block-wise diffusion denoising with confidence-based
+  sampling: repeated draft passes over a block that commit masked positions by
+  a confidence threshold, then a causal K/V refresh of the completed block
+  (its readings are listed with those functions at the end of this module).
 
 Readings where the paper is silent or its indices do not close (listed with
 reasons in the design notes of the repository):
@@ -372,3 +376,105 @@ def prefill(weights, kv, prefix_tokens, chunk: int = 0):
         blk = prefix_tokens[:, c0:c0 + chunk]
         _, nk, nv = block_forward(weights, kv, blk, VERIFY)
         commit(kv, nk, nv, np.full(kv.batch, blk.shape[1]))
+
+
+# ----------------------------------------------------------------------------- Mode 2: diffusion denoising
+# Block-wise diffusion decoding with confidence-based sampling (Sec. 3.2): a block
+# starts as masks after the verified prefix, each denoising step is one draft pass
+# over the block that commits some masked positions, and once no mask is left the
+# block's K/V is refreshed and decoding moves to the next block.
+#
+# Readings (the paper names the procedure and cites its source for the details):
+#
+# * Block layout as in Mode 3: ``[anchor, r_1 .. r_{k-1}]`` with the anchor at
+#   position P (its K/V not yet cached); r_j is a mask or a token committed by an
+#   earlier step, and a step over the block denoises the masked r_j in place.
+# * A masked position is denoised to the most probable token other than the mask
+#   token itself (a mask is never a decoded value); its confidence is that token's
+#   softmax probability over the same vocabulary (all tokens except the mask).
+# * Commit rule: every masked position whose confidence exceeds the threshold
+#   (strictly); when none does, the single most confident one (the lowest row
+#   among equal confidences), so each step commits at least one position -- the
+#   fallback the SOL construction of Sec. 4.1 also states for greedy acceptance.
+# * Refresh: the clean stream is strictly causal (Sec. 2.2), so a completed block's
+#   K/V is recomputed by a causal (verify-mode) pass over it.  Rows 0..k-2 (the
+#   anchor and the first k-2 decoded tokens) are committed; the last decoded token
+#   becomes the next block's anchor, as after a full acceptance in Mode 3.
+def denoising_logits(logits: np.ndarray, mask_id: int) -> np.ndarray:
+    """The logits over which a masked position is denoised: the mask token's own logit removed (-inf)."""
+    z = np.array(logits, dtype=np.float64, copy=True)
+    z[..., mask_id] = -np.inf
+    return z
+
+
+def top1_confidence(logits: np.ndarray) -> np.ndarray:
+    """Softmax probability of the most probable token, float64: 1 / sum_v exp(z_v - max_v z_v).
+
+    Entries at -inf take no part (probability 0)."""
+    z = np.asarray(logits, dtype=np.float64)
+    m = np.max(z, axis=-1, keepdims=True)
+    return 1.0 / np.sum(np.exp(z - m), axis=-1)
+
+
+def threshold_commit(block: np.ndarray, pred: np.ndarray, conf: np.ndarray, threshold: float, mask_id: int):
+    """One denoising step's commit for one sequence.
+
+    block: int [k] (row 0 the anchor, rows >= 1 a committed token or ``mask_id``);
+    pred/conf: per-row denoised token and its confidence.  Returns (new block,
+    sorted list of the rows committed by this step).
+    """
+    block = np.asarray(block)
+    masked = [j for j in range(1, len(block)) if block[j] == mask_id]
+    chosen = [j for j in masked if conf[j] > threshold]
+    if masked and not chosen:
+        best = masked[0]
+        for j in masked[1:]:
+            if conf[j] > conf[best]:
+                best = j
+        chosen = [best]
+    out = block.copy()
+    for j in chosen:
+        out[j] = pred[j]
+    return out, chosen
+
+
+def denoise_step(weights, kv, block: np.ndarray, threshold: float, bidir_from: int = 0):
+    """One denoising step for every sequence: a draft (bidirectional) pass over the current block, then
+    the commit rule.  The cache is not modified.  Returns dict with the new block, committed rows per
+    sequence, per-row prediction and confidence, and the pass's raw logits."""
+    mask_id = weights.shape.mask_token_id
+    block = np.asarray(block, dtype=np.int32)
+    logits, _, _ = block_forward(weights, kv, block, DRAFT, bidir_from)
+    z = denoising_logits(logits, mask_id)
+    pred = argmax_first(z)
+    conf = top1_confidence(z)
+    new_block = block.copy()
+    committed = []
+    for b in range(block.shape[0]):
+        new_block[b], rows = threshold_commit(block[b], pred[b], conf[b], threshold, mask_id)
+        committed.append(rows)
+    return {"block": new_block, "committed": committed, "pred": pred, "conf": conf, "logits": logits}
+
+
+def refresh(weights, kv, block: np.ndarray) -> np.ndarray:
+    """K/V refresh of completed blocks: a causal pass over ``block`` whose rows 0..k-2 are committed to
+    ``kv``.  Returns the next anchors (the blocks' last tokens)."""
+    block = np.asarray(block, dtype=np.int32)
+    B, k = block.shape
+    if np.any(block[:, 1:] == weights.shape.mask_token_id):
+        raise ValueError("refresh of a block that still holds a mask")
+    _, nk, nv = block_forward(weights, kv, block, VERIFY)
+    commit(kv, nk, nv, np.full(B, k - 1))
+    return block[:, k - 1].copy()
+
+
+def diffusion_block(weights, kv, anchor, k: int, threshold: float, bidir_from: int = 0):
+    """Mode 2 over one block per sequence: denoising steps until no mask is left, then the refresh.
+
+    Returns (decoded block [batch, k], number of denoising steps, next anchors)."""
+    block = draft_block(np.asarray(anchor), k, weights.shape.mask_token_id)
+    steps = 0
+    while np.any(block[:, 1:] == weights.shape.mask_token_id):
+        block = denoise_step(weights, kv, block, threshold, bidir_from)["block"]
+        steps += 1
+    return block, steps, refresh(weights, kv, block)

@@ -352,3 +352,148 @@ def test_chunked_prefill_equals_single_pass():
     for l in range(MINI.n_layers):
         np.testing.assert_allclose(a.k[l], b.k[l], rtol=1e-10, atol=1e-12)
         np.testing.assert_allclose(a.v[l], b.v[l], rtol=1e-10, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- Mode 2: diffusion denoising
+def test_top1_confidence_closed_forms():
+    """Confidence is the softmax probability of the top token: 1/V for equal logits, 3/4 for logits
+    (log 3, 0), 1/2 for two equal maxima with the rest excluded, invariant to a shift, and equal to the
+    maximum of torch's softmax on random rows."""
+    V = 97
+    np.testing.assert_allclose(O.top1_confidence(np.zeros((2, V))), 1.0 / V, rtol=1e-15)
+    np.testing.assert_allclose(O.top1_confidence(np.array([np.log(3.0), 0.0])), 0.75, rtol=1e-15)
+    z = np.full(V, -np.inf)
+    z[[4, 60]] = 1.5
+    np.testing.assert_allclose(O.top1_confidence(z), 0.5, rtol=1e-15)
+    rng = np.random.default_rng(3)
+    r = rng.standard_normal((5, V)) * 4
+    np.testing.assert_allclose(O.top1_confidence(r + 123.25), O.top1_confidence(r), rtol=1e-13)
+    lib = torch.softmax(torch.from_numpy(r), dim=-1).max(dim=-1).values.numpy()
+    np.testing.assert_allclose(O.top1_confidence(r), lib, rtol=1e-13)
+
+
+def test_denoising_never_decodes_the_mask_token():
+    """With the mask token's logit the largest of its row, the denoised token is the best other token and
+    its confidence is the softmax over the vocabulary without the mask token (torch on the reduced row)."""
+    V, mask_id = 50, 49
+    rng = np.random.default_rng(4)
+    r = rng.standard_normal((3, V))
+    r[:, mask_id] = 10.0
+    z = O.denoising_logits(r, mask_id)
+    assert np.all(O.argmax_first(z) == np.argmax(r[:, :mask_id], axis=-1))
+    lib = torch.softmax(torch.from_numpy(r[:, :mask_id]), dim=-1).max(dim=-1).values.numpy()
+    np.testing.assert_allclose(O.top1_confidence(z), lib, rtol=1e-13)
+
+
+@pytest.mark.parametrize("threshold", [-1.0, 0.0, 0.3, 0.5, 0.7, 0.95, 1.0])
+def test_threshold_commit_exhaustive(threshold):
+    """Every mask pattern of a k=5 block and every assignment of confidences from a small set (ties
+    included): the committed rows are exactly the masked rows above the threshold, or else the first of
+    the most confident masked rows; other rows and the anchor keep their tokens."""
+    M = 99
+    levels = [0.1, 0.5, 0.9]
+    for pattern in itertools.product([False, True], repeat=4):
+        block = np.array([7] + [M if m else 20 + j for j, m in enumerate(pattern)])
+        pred = np.array([0, 31, 32, 33, 34])
+        for cs in itertools.product(levels, repeat=4):
+            conf = np.array([0.0] + list(cs))
+            out, rows = O.threshold_commit(block, pred, conf, threshold, M)
+            masked = [j for j in range(1, 5) if pattern[j - 1]]
+            above = [j for j in masked if conf[j] > threshold]
+            if above:
+                assert rows == above
+            elif masked:
+                top = max(conf[j] for j in masked)
+                assert rows == [min(j for j in masked if conf[j] == top)]
+            else:
+                assert rows == []
+            for j in range(5):
+                assert out[j] == (pred[j] if j in rows else block[j])
+
+
+def test_threshold_commit_monotone_in_threshold():
+    """A lower threshold commits a superset of the rows a higher one commits (when both commit by
+    threshold), and a threshold of 1 or more commits exactly one row per step."""
+    rng = np.random.default_rng(5)
+    M = 1000
+    for _ in range(200):
+        k = int(rng.integers(2, 12))
+        block = np.where(rng.random(k) < 0.7, M, 5)
+        block[0] = 3
+        conf = rng.random(k)
+        pred = rng.integers(0, M, k)
+        hi_rows = O.threshold_commit(block, pred, conf, 0.8, M)[1]
+        lo_rows = O.threshold_commit(block, pred, conf, 0.4, M)[1]
+        if any(conf[j] > 0.8 for j in hi_rows):
+            assert set(hi_rows) <= set(lo_rows)
+        n_masked = int(np.sum(block[1:] == M))
+        assert len(O.threshold_commit(block, pred, conf, 1.0, M)[1]) == min(1, n_masked)
+
+
+@pytest.fixture(scope="module")
+def mode2():
+    w = mini_weights()
+    prefix = synth_tokens(MINI, 14, "pin.m2.prefix", (2, 11))
+    return w, prefix
+
+
+def test_diffusion_threshold_below_zero_is_one_draft_pass(mode2):
+    """With every confidence above the threshold the block is decoded in one step, to the argmax (mask
+    token excluded) of one draft pass over [anchor, masks] -- the Mode 3 draft pass."""
+    w, prefix = mode2
+    k = 6
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    logits, _, _ = O.block_forward(w, kv, O.draft_block(prefix[:, -1], k, MINI.mask_token_id), O.DRAFT)
+    expect = np.argmax(np.where(np.arange(MINI.vocab) == MINI.mask_token_id, -np.inf, logits), axis=-1)[:, 1:]
+    block, steps, nxt = O.diffusion_block(w, kv, prefix[:, -1], k, threshold=-1.0)
+    assert steps == 1
+    np.testing.assert_array_equal(block[:, 1:], expect)
+    np.testing.assert_array_equal(block[:, 0], prefix[:, -1])
+    np.testing.assert_array_equal(nxt, block[:, -1])
+
+
+def test_diffusion_threshold_one_decodes_one_token_per_step(mode2):
+    """A threshold no probability exceeds gives one commit per step (k-1 steps), each the most confident
+    remaining mask -- decoding one token at a time in confidence order."""
+    w, prefix = mode2
+    k = 5
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    block = O.draft_block(prefix[:, -1], k, MINI.mask_token_id)
+    for step in range(k - 1):
+        r = O.denoise_step(w, kv, block, threshold=1.0)
+        for b in range(2):
+            assert len(r["committed"][b]) == 1
+            j = r["committed"][b][0]
+            masked = [i for i in range(1, k) if block[b, i] == MINI.mask_token_id]
+            assert j in masked and r["conf"][b, j] == max(r["conf"][b, i] for i in masked)
+        block = r["block"]
+    assert not np.any(block == MINI.mask_token_id)
+    assert np.all(kv.lengths == prefix.shape[1] - 1)            # denoising never writes the cache
+
+
+@pytest.mark.parametrize("threshold", [0.02, 0.05, 0.2])
+def test_diffusion_refresh_equals_causal_recompute(mode2, threshold):
+    """After a block is decoded and refreshed the cache holds P + k - 1 rows, the next anchor is the
+    block's last token, and an AR step from it equals plain causal decoding recomputed from all tokens
+    (no cache).  Any threshold finishes the block in at most k - 1 steps."""
+    w, prefix = mode2
+    k = 6
+    P = prefix.shape[1] - 1
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    block, steps, nxt = O.diffusion_block(w, kv, prefix[:, -1], k, threshold)
+    assert 1 <= steps <= k - 1
+    assert np.all(kv.lengths == P + k - 1)
+    np.testing.assert_array_equal(nxt, block[:, -1])
+    tok_ar, logits_ar = O.ar_step(w, kv, nxt)
+    seq = np.concatenate([prefix[:, :-1], block], axis=1)
+    T = seq.shape[1]
+    full = O.full_forward(w, seq, np.tril(np.ones((T, T), dtype=bool)))
+    np.testing.assert_allclose(logits_ar[:, 0], full[:, -1], rtol=1e-10, atol=1e-12)
+    np.testing.assert_array_equal(tok_ar, O.argmax_first(full[:, -1]))
+
+
+def test_refresh_rejects_an_incomplete_block(mode2):
+    w, prefix = mode2
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    with pytest.raises(ValueError):
+        O.refresh(w, kv, O.draft_block(prefix[:, -1], 4, MINI.mask_token_id))
