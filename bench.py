@@ -10,6 +10,9 @@ device).  The timed steps replay one captured HIP graph.
 
 value = block tokens pushed through block-decode passes per second
       = 2 passes x batch x k per step / step time.
+Also timed (reported under "mode2", not part of value): one Mode 2 denoising step
+over [anchor, mask x (k-1)] at threshold 0.9 and one K/V refresh of a completed
+block, each replayed from its own captured graph.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -55,6 +58,58 @@ def pass_bytes(shape, batch, k, prefix_lens):
     kb = kernel_bytes(shape, batch, k, prefix_lens)
     return kb["embed"] + shape.n_layers * (kb["qkv"] + kb["attention"] + kb["o_proj"] + kb["gate_up"] + kb["down"]) \
         + kb["lm_head"]
+
+
+def refresh_bytes(shape, batch, k, prefix_lens):
+    """A refresh runs every layer's QKV but stops after the last one: no attention, FFN or LM head after it."""
+    kb = kernel_bytes(shape, batch, k, prefix_lens)
+    return kb["embed"] + shape.n_layers * kb["qkv"] \
+        + (shape.n_layers - 1) * (kb["attention"] + kb["o_proj"] + kb["gate_up"] + kb["down"])
+
+
+def mode2_timing(R, model, cache, ws, anchor, block_full, k, reps, threshold=0.9):
+    """Mean ms of one denoising step (block reset to [anchor, masks] first) and of one refresh (lengths reset
+    first, so every replay refreshes the same rows), each from a captured graph replayed `reps` times."""
+    import torch
+    B = anchor.shape[0]
+    dev = anchor.device
+    blk0 = torch.full((B, k), model.shape.mask_token_id, dtype=torch.int32, device=dev)
+    blk0[:, 0] = anchor
+    blk = blk0.clone()
+    outs = {"n_committed": torch.empty(B, dtype=torch.int32, device=dev),
+            "n_masked": torch.empty(B, dtype=torch.int32, device=dev),
+            "confidence": torch.empty((B, k), dtype=torch.float32, device=dev)}
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    len0 = cache.lengths.clone()
+
+    def denoise():
+        blk.copy_(blk0)
+        R.denoise_step(model, cache, ws, blk, threshold, outs=outs)
+
+    def refresh():
+        cache.lengths.copy_(len0)
+        R.refresh_block(model, cache, ws, block_full, next_anchor=nxt)
+
+    res = {}
+    for name, fn in (("denoise_step", denoise), ("refresh", refresh)):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=torch.cuda.current_stream()):
+            fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / reps
+    committed = int(outs["n_committed"].sum().item())
+    cache.lengths.copy_(len0)
+    torch.cuda.synchronize()
+    return res, committed
 
 
 def blas_threads():
@@ -169,7 +224,7 @@ def main():
     shape, k, B = wl.shape, wl.k_values[0], wl.batch
     plens = wl.prefix_lengths()
     steps, warmup = args.steps, args.warmup
-    max_len = int(-(-(int(plens.max()) + (steps + warmup + 4) * k) // 64) * 64)
+    max_len = int(-(-(int(plens.max()) + (steps + warmup + 6) * k) // 64) * 64)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
@@ -237,6 +292,10 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
+        block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
+        m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
+        status |= R.read_device_status(ws)
+
     ms_per_step = elapsed_ms / steps
     value = 2.0 * B * k / (ms_per_step * 1e-3)
     bytes_step = 2 * pass_bytes(shape, B, k, plens)
@@ -280,6 +339,16 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "bytes_per_launch": int(kb[dom]), "avg_launch_us": kernels[dom]["avg_us"]},
         "kernels": kernels,
+        "mode2": {
+            "denoise_step_ms": round(m2_ms["denoise_step"], 4),
+            "denoise_hbm_frac": round(pass_bytes(shape, B, k, plens) / (m2_ms["denoise_step"] * 1e-3) / 1e9
+                                      / HBM_PEAK_GBS, 4),
+            "refresh_ms": round(m2_ms["refresh"], 4),
+            "refresh_hbm_frac": round(refresh_bytes(shape, B, k, plens) / (m2_ms["refresh"] * 1e-3) / 1e9
+                                      / HBM_PEAK_GBS, 4),
+            "threshold": 0.9,
+            "first_step_commits": m2_committed,
+        },
     }
     if not args.no_cpu_baseline:
         del model, cache, ws

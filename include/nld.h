@@ -63,6 +63,7 @@ typedef enum {
 #define NLD_DEV_BAD_TOKEN 0x1u     /* a token id outside [0, vocab) was replaced by 0 */
 #define NLD_DEV_CAPACITY 0x2u      /* P_b + k > max_len: the block's K/V rows were not written */
 #define NLD_DEV_BAD_LENGTH 0x4u    /* a negative committed length was read */
+#define NLD_DEV_MASK_LEFT 0x8u     /* nld_refresh_block found a mask token in block rows 1..k-1 */
 
 typedef enum {
     NLD_MODE_VERIFY = 0,   /* AR verify: causal within the block */
@@ -112,8 +113,9 @@ typedef struct {
  * lengths[b] = P_b, the committed length of sequence b.  Rows at positions
  * >= P_b are scratch: a verify pass writes its block's K/V rows to positions
  * [P_b, P_b + k) (a draft pass writes no cache row), and only
- * nld_verify_accept advances lengths (by L+1), which commits the anchor row
- * and the accepted draft rows; the rest are overwritten by later passes.
+ * nld_verify_accept (by L+1: the anchor row and the accepted draft rows) and
+ * nld_refresh_block (by k-1) advance lengths, which commits those rows; the
+ * rest are overwritten by later passes.
  * Within a pass the block attends to its own keys and values from a
  * higher-precision copy in the workspace (bf16 value plus bf16 remainder),
  * so the cache rows are only what a commit keeps. */
@@ -214,6 +216,53 @@ size_t nld_accept_workspace_bytes(int32_t batch, int32_t k);
 nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int32_t batch, int32_t k,
                                   int32_t vocab, int32_t* argmax, int32_t* accept_len, int32_t* committed,
                                   int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- Mode 2: block-wise diffusion denoising (Sec. 3.2) -----------------------
+ * Confidence-based decoding of one block per sequence: the block starts as
+ * [anchor, mask x (k-1)] and each denoising step, one diffusion (draft) pass
+ * over the current block, fills in some of its masked rows; when no mask is
+ * left, a refresh recomputes the block's K/V with the causal mask (the clean
+ * stream is strictly causal, Sec. 2.2) and commits it, and the next block
+ * starts from the last decoded token as its anchor.
+ * A masked row is denoised to the argmax of its logits over every token except
+ * mask_token_id (a mask is never a decoded value), with confidence = that
+ * token's softmax probability over the same tokens. */
+
+/* One denoising step.  block: int32 [batch][k], in/out; row 0 is the anchor,
+ * rows 1..k-1 hold mask_token_id (still masked) or an earlier step's token.
+ * Runs the draft pass (rows >= bidir_from see every block column) and commits,
+ * per sequence, every masked row whose confidence exceeds `threshold`
+ * (strictly); when none does, the most confident masked row (the lowest row
+ * among equal confidences), so a step with a mask left commits at least one.
+ * Writes n_committed[b] (rows filled by this step) and n_masked[b] (masks
+ * left); confidence (optional) f32 [batch][k] gets every row's confidence and
+ * logits (optional) the pass's raw logits.  The cache and lengths are not
+ * touched.  A block with no mask left is returned unchanged (n_committed 0).
+ * Errors as nld_block_forward, plus INVALID_ARG for k < 2, a NULL
+ * block/n_committed/n_masked or a NaN threshold. */
+nld_status nld_denoise_step(const nld_model* m, const nld_kv_cache* kv, int32_t* block, int32_t batch, int32_t k,
+                            int32_t bidir_from, float threshold, int32_t* n_committed, int32_t* n_masked,
+                            float* confidence, float* logits, void* workspace, size_t ws_bytes, void* stream);
+
+/* K/V refresh of completed blocks: a causal pass over block [batch][k] that
+ * writes every layer's K/V rows [P_b, P_b + k) and then commits k-1 of them
+ * (lengths[b] += k-1: the anchor and rows 1..k-2), with next_anchor[b] =
+ * block[b][k-1].  Only the K/V projections run in the last layer and the LM
+ * head does not run (nothing after the last K/V write is needed).  A mask
+ * token left in rows 1..k-1 sets NLD_DEV_MASK_LEFT (the rows are still
+ * committed).  Errors as nld_block_forward, plus INVALID_ARG for k < 2. */
+nld_status nld_refresh_block(const nld_model* m, const nld_kv_cache* kv, const int32_t* block, int32_t batch,
+                             int32_t k, int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream);
+
+/* The denoising step's decision alone, from given logits f32 [batch][k][vocab]:
+ * argmax (optional) int32 [batch][k] and confidence (optional) f32 [batch][k]
+ * over the tokens other than mask_token_id, and the same in-place commit into
+ * block [batch][k] with n_committed / n_masked as nld_denoise_step.  Needs no
+ * workspace.  Errors: INVALID_ARG (NULL pointer, batch < 1, k outside [2, 64],
+ * vocab < 2, mask_token_id outside [0, vocab), NaN threshold). */
+nld_status nld_commit_from_logits(const float* logits, int32_t* block, int32_t batch, int32_t k, int32_t vocab,
+                                  int32_t mask_token_id, float threshold, int32_t* argmax, int32_t* n_committed,
+                                  int32_t* n_masked, float* confidence, void* stream);
 
 /* ---- tracing aid -------------------------------------------------------------
  * While enabled, every kernel launch made by the block-decode calls is

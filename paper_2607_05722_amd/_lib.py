@@ -22,6 +22,7 @@ NLD_MODE_DRAFT = 1
 NLD_DEV_BAD_TOKEN = 0x1
 NLD_DEV_CAPACITY = 0x2
 NLD_DEV_BAD_LENGTH = 0x4
+NLD_DEV_MASK_LEFT = 0x8
 
 NLD_PACK_LINEAR = 0
 NLD_PACK_QKV = 1
@@ -31,7 +32,8 @@ EXPORTED = [
     "nld_last_error", "nld_status_string", "nld_model_create", "nld_model_destroy", "nld_packed_bytes",
     "nld_pack_linear", "nld_pack_qkv", "nld_pack_gate_up", "nld_workspace_bytes", "nld_workspace_init",
     "nld_block_forward", "nld_draft", "nld_verify_accept", "nld_accept_workspace_bytes",
-    "nld_accept_from_logits", "nld_read_device_status", "nld_trace_enable", "nld_trace_read",
+    "nld_accept_from_logits", "nld_denoise_step", "nld_refresh_block", "nld_commit_from_logits",
+    "nld_read_device_status", "nld_trace_enable", "nld_trace_read",
 ]
 
 TRACE_CLASSES = ["embed", "qkv", "attention", "o_proj", "gate_up", "down", "lm_head", "argmax"]
@@ -114,6 +116,13 @@ def load():
     L.nld_accept_workspace_bytes.argtypes = [c_i32, c_i32]
     L.nld_accept_from_logits.restype = c_i32
     L.nld_accept_from_logits.argtypes = [c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.nld_denoise_step.restype = c_i32
+    L.nld_denoise_step.argtypes = [c_vp, P(KVCache), c_vp, c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                   c_sz, c_vp]
+    L.nld_refresh_block.restype = c_i32
+    L.nld_refresh_block.argtypes = [c_vp, P(KVCache), c_vp, c_i32, c_i32, c_vp, c_vp, c_sz, c_vp]
+    L.nld_commit_from_logits.restype = c_i32
+    L.nld_commit_from_logits.argtypes = [c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp]
     L.nld_read_device_status.restype = c_i32
     L.nld_read_device_status.argtypes = [c_vp, P(c_u32), c_vp]
     L.nld_trace_enable.restype = c_i32

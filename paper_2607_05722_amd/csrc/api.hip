@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, rope, po, pml, blk_k, blk_v, tile_ctr, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -119,6 +119,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.o = take(4 * L.Mpad * QD);
     L.act = take(4 * L.Mpad * (size_t)cdiv(c.ffn, 32) * 32);
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
+    L.lse = take(8 * L.Mpad * (size_t)L.lm_parts);   // softmax statistics per argmax partial (denoising)
     L.rope = take(8 * L.Mpad * (size_t)(c.head_dim / 2));
     L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1));   // per pass: QKV and gate/up of every layer, LM head
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
@@ -211,6 +212,13 @@ struct PassIO {
     int32_t* committed;
     int32_t* next_anchor;
     bool advance_lengths;
+    // denoising step / refresh
+    int32_t* block;
+    float threshold;
+    int32_t* n_committed;
+    int32_t* n_masked;
+    float* conf_out;
+    bool kv_only;   // refresh: stop after the last layer's K/V (no attention, FFN or LM head after it)
 };
 
 nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, int k, void* ws, size_t ws_bytes,
@@ -321,6 +329,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
             TraceScope ts(NLD_TRACE_QKV, s);
             HIP_TRY(normed_gemm(EPI_QKV, g, ws, L, s, nullptr));
         }
+        if (io.kv_only && l == c.n_layers - 1) break;   // every layer's K/V rows are written
 
         AttnArgs at_{};
         at_.q = at<uint16_t>(ws, L.q);
@@ -400,6 +409,22 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         }
     }
 
+    FinishArgs fa{};
+    fa.k_blk = k;
+    fa.batch = batch;
+    fa.finish = io.finish;
+    fa.status = status;
+    fa.mask_id = c.mask_token_id;
+    if (io.kv_only) {
+        fa.block = io.block;
+        fa.next_anchor = io.next_anchor;
+        fa.lengths = kv->lengths;
+        TraceScope ts(NLD_TRACE_ARGMAX, s);
+        HIP_TRY(launch_finish(fa, s));
+        return NLD_OK;
+    }
+
+    const bool denoise = io.finish == FINISH_DENOISE;
     GemmArgs gl{};
     gl.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * c.n_layers;
     gl.eps = c.rms_eps;
@@ -410,6 +435,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     gl.ksteps = ks_h;
     gl.logits = io.logits;
     gl.part_keys = at<unsigned long long>(ws, L.keys);
+    gl.part_lse = denoise ? at<float2>(ws, L.lse) : nullptr;
+    gl.exclude_id = denoise ? c.mask_token_id : -1;
     gl.vocab = c.vocab;
     int parts = 0;
     {
@@ -417,14 +444,16 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         HIP_TRY(normed_gemm(EPI_LMHEAD, gl, ws, L, s, &parts));
     }
 
-    FinishArgs fa{};
     fa.part_keys = at<unsigned long long>(ws, L.keys);
+    fa.part_lse = at<float2>(ws, L.lse);
     fa.n_parts = parts;
     fa.vocab = c.vocab;
-    fa.k_blk = k;
-    fa.batch = batch;
     fa.argmax_out = io.argmax_out;
-    fa.finish = io.finish;
+    fa.block = io.block;
+    fa.threshold = io.threshold;
+    fa.n_committed = io.n_committed;
+    fa.n_masked = io.n_masked;
+    fa.conf_out = io.conf_out;
     fa.draft_in = io.draft_in;
     fa.draft_out = io.draft_out;
     fa.accept_len = io.accept_len;
@@ -622,6 +651,74 @@ nld_status nld_verify_accept(const nld_model* m, const nld_kv_cache* kv, const i
     io.next_anchor = next_anchor;
     io.advance_lengths = true;
     return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+nld_status nld_denoise_step(const nld_model* m, const nld_kv_cache* kv, int32_t* block, int32_t batch, int32_t k,
+                            int32_t bidir_from, float threshold, int32_t* n_committed, int32_t* n_masked,
+                            float* confidence, float* logits, void* workspace, size_t ws_bytes, void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (k < 2) return fail(NLD_ERR_INVALID_ARG, "a denoising step needs k >= 2");
+    if (m->cfg.vocab < 2) return fail(NLD_ERR_SHAPE, "denoising needs a vocabulary besides the mask token");
+    if (!block || !n_committed || !n_masked) return fail(NLD_ERR_INVALID_ARG, "block, n_committed or n_masked is NULL");
+    if (bidir_from < 0 || bidir_from > k) return fail(NLD_ERR_INVALID_ARG, "bidir_from must be in [0, k]");
+    if (threshold != threshold) return fail(NLD_ERR_INVALID_ARG, "threshold is NaN");
+    PassIO io{};
+    io.source = SRC_TOKENS;
+    io.tokens = block;
+    io.mode = NLD_MODE_DRAFT;
+    io.bidir_from = bidir_from;
+    io.logits = logits;
+    io.finish = FINISH_DENOISE;
+    io.block = block;
+    io.threshold = threshold;
+    io.n_committed = n_committed;
+    io.n_masked = n_masked;
+    io.conf_out = confidence;
+    return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+nld_status nld_refresh_block(const nld_model* m, const nld_kv_cache* kv, const int32_t* block, int32_t batch,
+                             int32_t k, int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (k < 2) return fail(NLD_ERR_INVALID_ARG, "a refresh needs k >= 2");
+    if (!block || !next_anchor) return fail(NLD_ERR_INVALID_ARG, "block or next_anchor is NULL");
+    PassIO io{};
+    io.source = SRC_TOKENS;
+    io.tokens = block;
+    io.mode = NLD_MODE_VERIFY;
+    io.finish = FINISH_REFRESH;
+    io.block = (int32_t*)block;   // read only
+    io.next_anchor = next_anchor;
+    io.kv_only = true;
+    return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+nld_status nld_commit_from_logits(const float* logits, int32_t* block, int32_t batch, int32_t k, int32_t vocab,
+                                  int32_t mask_token_id, float threshold, int32_t* argmax, int32_t* n_committed,
+                                  int32_t* n_masked, float* confidence, void* stream) {
+    if (!logits || !block || !n_committed || !n_masked) return fail(NLD_ERR_INVALID_ARG, "NULL pointer");
+    if (batch < 1 || k < 2 || k > 64 || vocab < 2) return fail(NLD_ERR_INVALID_ARG, "bad batch, k or vocab");
+    if (mask_token_id < 0 || mask_token_id >= vocab) return fail(NLD_ERR_INVALID_ARG, "mask_token_id outside [0, vocab)");
+    if (threshold != threshold) return fail(NLD_ERR_INVALID_ARG, "threshold is NaN");
+    FinishArgs fa{};
+    fa.logits = logits;
+    fa.vocab = vocab;
+    fa.k_blk = k;
+    fa.batch = batch;
+    fa.argmax_out = argmax;
+    fa.finish = FINISH_DENOISE;
+    fa.block = block;
+    fa.mask_id = mask_token_id;
+    fa.threshold = threshold;
+    fa.n_committed = n_committed;
+    fa.n_masked = n_masked;
+    fa.conf_out = confidence;
+    HIP_TRY(launch_finish(fa, (hipStream_t)stream));
+    return NLD_OK;
 }
 
 size_t nld_accept_workspace_bytes(int32_t batch, int32_t k) {

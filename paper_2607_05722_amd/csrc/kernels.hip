@@ -27,6 +27,7 @@ namespace nld {
 static constexpr uint32_t DEV_BAD_TOKEN = 0x1u;
 static constexpr uint32_t DEV_CAPACITY = 0x2u;
 static constexpr uint32_t DEV_BAD_LENGTH = 0x4u;
+static constexpr uint32_t DEV_MASK_LEFT = 0x8u;
 
 __device__ __forceinline__ int committed_length(const int32_t* lengths, int b, int max_len, uint32_t* status) {
     int p = lengths[b];
@@ -106,15 +107,36 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, float y, int m, in
     }
 }
 
-// Returns, in every lane, the argmax key of row m over this tile's 16 columns.
-__device__ __forceinline__ unsigned long long epi_lmhead(const GemmArgs& a, float y, int m, int t, int lane) {
+// Softmax statistics as (max, sum of exp(z - max)); (-inf, 0) is the empty set.
+__device__ __forceinline__ float2 lse_merge(float2 a, float2 b) {
+    if (b.x == -INFINITY) return a;
+    if (a.x == -INFINITY) return b;
+    const float mx = fmaxf(a.x, b.x);
+    return float2{mx, a.y * expf(a.x - mx) + b.y * expf(b.x - mx)};
+}
+
+// Returns, in every lane, the argmax key of row m over this tile's 16 columns and,
+// when the pass asks for softmax statistics, the tile row's (max, sum of exp) in
+// *lse.  The excluded column (the mask token when denoising) takes part in neither.
+__device__ __forceinline__ unsigned long long epi_lmhead(const GemmArgs& a, float y, int m, int t, int lane,
+                                                         float2* lse) {
     const int r = lane & 15;
     const int n = t * 16 + r;
-    const bool ok = m < a.M && n < a.vocab;
-    if (ok && a.logits) a.logits[(size_t)m * a.vocab + n] = y;
+    const bool in = m < a.M && n < a.vocab;
+    const bool ok = in && n != a.exclude_id;
+    if (in && a.logits) a.logits[(size_t)m * a.vocab + n] = y;
     unsigned long long key = ok ? argmax_key(y, (uint32_t)n) : 0ull;
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) key = umax64(key, __shfl_xor(key, off));
+    if (a.part_lse) {
+        float mx = ok ? y : -INFINITY;
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        float e = ok ? expf(y - mx) : 0.f;
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) e += __shfl_xor(e, off);
+        *lse = float2{mx, e};
+    }
     return key;
 }
 
@@ -172,13 +194,17 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     __shared__ f32x4_t red[2][16][64];
     __shared__ float inv_s[16];
     __shared__ unsigned long long key_s[16][16];
+    __shared__ float2 lse_s[16][16];
     __shared__ int pos_s[16];
 
     __shared__ int next_s[2];
 
     const int NW = blockDim.x >> 6;
     if constexpr (EPI == EPI_LMHEAD) {
-        if (threadIdx.x < 256) key_s[threadIdx.x >> 4][threadIdx.x & 15] = 0ull;
+        if (threadIdx.x < 256) {
+            key_s[threadIdx.x >> 4][threadIdx.x & 15] = 0ull;
+            lse_s[threadIdx.x >> 4][threadIdx.x & 15] = float2{-INFINITY, 0.f};
+        }
     }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -250,8 +276,12 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
                 if constexpr (EPI == EPI_QKV) epi_qkv(a, y, m, t, lane, pos_s[m]);
                 else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, y, m, t, lane);
                 else {
-                    const unsigned long long key = epi_lmhead(a, y, m, t, lane);
-                    if (r == 0) key_s[wave][m] = umax64(key_s[wave][m], key);
+                    float2 tl;
+                    const unsigned long long key = epi_lmhead(a, y, m, t, lane, &tl);
+                    if (r == 0) {
+                        key_s[wave][m] = umax64(key_s[wave][m], key);
+                        if (a.part_lse) lse_s[wave][m] = lse_merge(lse_s[wave][m], tl);
+                    }
                 }
             }
         }
@@ -264,6 +294,11 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
             unsigned long long best = 0ull;
             for (int w = 0; w < NW; ++w) best = umax64(best, key_s[w][threadIdx.x]);
             a.part_keys[(size_t)threadIdx.x * a.n_parts + blockIdx.x] = best;
+            if (a.part_lse) {
+                float2 st = float2{-INFINITY, 0.f};
+                for (int w = 0; w < NW; ++w) st = lse_merge(st, lse_s[w][threadIdx.x]);
+                a.part_lse[(size_t)threadIdx.x * a.n_parts + blockIdx.x] = st;
+            }
         }
     }
 }
@@ -320,6 +355,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     constexpr int BSTRIDE = SPLIT ? 1024 : 512;   // elements per (row tile, k-step) block
     __shared__ f32x4_t red[NW][MT * CT][64];
     __shared__ unsigned long long key_s[16 * MT];
+    __shared__ float2 lse_s[16 * MT][CT];
     __shared__ float inv_s[16 * MT];
 
     const int lane = threadIdx.x & 63;
@@ -428,6 +464,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         for (int ct = 0; ct < CT; ++ct) red[wave][mt * CT + ct][lane] = acc[mt][ct];
     if constexpr (EPI == EPI_LMHEAD) {
         if (threadIdx.x < 16 * MT) key_s[threadIdx.x] = 0ull;
+        if (threadIdx.x < 16 * MT * CT) lse_s[threadIdx.x / CT][threadIdx.x % CT] = float2{-INFINITY, 0.f};
     }
     __syncthreads();
     for (int ti = ti0; ti < MT * CT; ti += GROUPS) {
@@ -454,15 +491,27 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         } else if constexpr (EPI == EPI_SWIGLU) {
             epi_swiglu(a, v * inv_s[ml], m, t, lane);
         } else {
-            const unsigned long long key = epi_lmhead(a, v * inv_s[ml], m, t, lane);
-            if (r == 0) atomicMax(&key_s[ml], key);
+            float2 tl;
+            const unsigned long long key = epi_lmhead(a, v * inv_s[ml], m, t, lane, &tl);
+            if (r == 0) {
+                atomicMax(&key_s[ml], key);
+                if (a.part_lse) lse_s[ml][ct] = tl;   // each (row, column tile) is finished once
+            }
         }
     }
     if constexpr (EPI == EPI_LMHEAD) {
         __syncthreads();
         if (threadIdx.x < 16 * MT) {
             const int m = m0 + threadIdx.x;
-            if (m < a.M) a.part_keys[(size_t)m * a.n_parts + blockIdx.x] = key_s[threadIdx.x];
+            if (m < a.M) {
+                a.part_keys[(size_t)m * a.n_parts + blockIdx.x] = key_s[threadIdx.x];
+                if (a.part_lse) {
+                    float2 st = float2{-INFINITY, 0.f};
+#pragma unroll
+                    for (int c = 0; c < CT; ++c) st = lse_merge(st, lse_s[threadIdx.x][c]);
+                    a.part_lse[(size_t)m * a.n_parts + blockIdx.x] = st;
+                }
+            }
         }
     }
 }
@@ -956,39 +1005,94 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
 // =====================================================================================
 // Per-sequence finish: argmax of each block row (from the LM head's per-workgroup
 // keys, or from given logits; lowest index among equal maxima), then draft
-// extraction (d_j = argmax of draft row j) or longest-prefix acceptance with the
-// bonus token and the commit of L+1 rows.  One workgroup per sequence, one
-// wavefront per row.
+// extraction (d_j = argmax of draft row j), longest-prefix acceptance with the
+// bonus token and the commit of L+1 rows, or a denoising step's commit: masked
+// rows whose top-1 softmax probability exceeds the threshold take their argmax,
+// else the most confident masked row does.  A refresh only commits k-1 rows.
+// One workgroup per sequence, one wavefront per row.
 // =====================================================================================
+// the float value an argmax key was made from
+__device__ __forceinline__ float argmax_key_value(unsigned long long key) {
+    const uint32_t ord = (uint32_t)(key >> 32);
+    return __uint_as_float((ord & 0x80000000u) ? (ord ^ 0x80000000u) : ~ord);
+}
+
 __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
     __shared__ int32_t am[64];
+    __shared__ float cf[64];
     const int b = blockIdx.x, k = a.k_blk;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const bool denoise = a.finish == FINISH_DENOISE;
+    if (a.finish == FINISH_REFRESH) {
+        if (threadIdx.x != 0) return;
+        const int32_t* blk = a.block + (size_t)b * k;
+        for (int j = 1; j < k; ++j)
+            if (blk[j] == a.mask_id) atomicOr(a.status, DEV_MASK_LEFT);
+        a.next_anchor[b] = blk[k - 1];
+        a.lengths[b] += k - 1;
+        return;
+    }
     for (int jr = wave; jr < k; jr += nw) {
         const int m = b * k + jr;
         unsigned long long best = 0ull;
+        float2 st = float2{-INFINITY, 0.f};   // softmax statistics (denoising only)
         if (a.part_keys) {
             const unsigned long long* pk = a.part_keys + (size_t)m * a.n_parts;
             int p = lane;
             for (; p + 192 < a.n_parts; p += 256)
                 best = umax64(umax64(best, pk[p]), umax64(umax64(pk[p + 64], pk[p + 128]), pk[p + 192]));
             for (; p < a.n_parts; p += 64) best = umax64(best, pk[p]);
+            if (denoise)
+                for (int q = lane; q < a.n_parts; q += 64) st = lse_merge(st, a.part_lse[(size_t)m * a.n_parts + q]);
         } else {
             const float* lg = a.logits + (size_t)m * a.vocab;
-            for (int n = lane; n < a.vocab; n += 64) best = umax64(best, argmax_key(lg[n], (uint32_t)n));
+            const int excl = denoise ? a.mask_id : -1;
+            for (int n = lane; n < a.vocab; n += 64) {
+                if (n == excl) continue;
+                const float v = lg[n];
+                best = umax64(best, argmax_key(v, (uint32_t)n));
+                if (denoise) st = lse_merge(st, float2{v, 1.f});
+            }
         }
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) best = umax64(best, __shfl_xor(best, off));
+        if (denoise) {
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                const float2 o = float2{__shfl_xor(st.x, off), __shfl_xor(st.y, off)};
+                st = lse_merge(st, o);
+            }
+        }
         if (lane == 0) {
             const int idx = argmax_key_index(best);
             am[jr] = idx;
             if (a.argmax_out) a.argmax_out[m] = idx;
+            if (denoise) {
+                // probability of the argmax token: exp(z_best - max) / sum (the max is z_best)
+                const float c = expf(argmax_key_value(best) - st.x) / st.y;
+                cf[jr] = c;
+                if (a.conf_out) a.conf_out[m] = c;
+            }
         }
     }
     __syncthreads();
     if (threadIdx.x != 0 || a.finish == FINISH_NONE) return;
     if (a.finish == FINISH_DRAFT) {
         for (int jj = 1; jj < k; ++jj) a.draft_out[(size_t)b * (k - 1) + jj - 1] = am[jj];
+    } else if (denoise) {
+        int32_t* blk = a.block + (size_t)b * k;
+        int n_mask = 0, n_above = 0, top = -1;
+        for (int j = 1; j < k; ++j) {
+            if (blk[j] != a.mask_id) continue;
+            ++n_mask;
+            if (cf[j] > a.threshold) ++n_above;
+            if (top < 0 || cf[j] > cf[top]) top = j;   // first of the most confident
+        }
+        for (int j = 1; j < k; ++j)
+            if (blk[j] == a.mask_id && (n_above > 0 ? cf[j] > a.threshold : j == top)) blk[j] = am[j];
+        const int n_commit = n_above > 0 ? n_above : (n_mask > 0 ? 1 : 0);
+        a.n_committed[b] = n_commit;
+        a.n_masked[b] = n_mask - n_commit;
     } else {
         const int32_t* dr = a.draft_in + (size_t)b * (k - 1);
         int L = 0;
@@ -1001,7 +1105,7 @@ __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
 }
 
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s) {
-    const int threads = 64 * (a.k_blk < 16 ? a.k_blk : 16);
+    const int threads = a.finish == FINISH_REFRESH ? 64 : 64 * (a.k_blk < 16 ? a.k_blk : 16);
     finish_kernel<<<a.batch, threads, 0, s>>>(a);
     return hipGetLastError();
 }

@@ -119,6 +119,8 @@ struct GemmArgs {
     // EPI_LMHEAD
     float* logits;                   // optional f32 [M][vocab]
     unsigned long long* part_keys;   // [M][n_parts]: one argmax key per row per workgroup
+    float2* part_lse;                // optional [M][n_parts]: (max, sum of exp(z - max)) per row per workgroup
+    int exclude_id;                  // column left out of the argmax and the sums (-1: none)
     int n_parts;
     int vocab;
 };
@@ -168,7 +170,7 @@ struct EmbedArgs {
     double inv_freq[64];    // base^(-2i/head_dim), computed on the host in fp64
 };
 
-enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2 };
+enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2, FINISH_DENOISE = 3, FINISH_REFRESH = 4 };
 
 struct FinishArgs {
     const unsigned long long* part_keys;  // [M][n_parts] (or NULL: reduce `logits`)
@@ -183,7 +185,16 @@ struct FinishArgs {
     int32_t* accept_len;
     int32_t* committed;                   // [batch][k]
     int32_t* next_anchor;
-    int32_t* lengths;                     // advanced by L+1 (may be NULL)
+    int32_t* lengths;                     // advanced by L+1 (may be NULL); FINISH_REFRESH: by k-1
+    // FINISH_DENOISE: confidence-threshold commit into `block`; FINISH_REFRESH: reads `block`
+    const float2* part_lse;               // [M][n_parts] (NULL with `logits`: reduced from them)
+    int32_t* block;                       // [batch][k]
+    int mask_id;                          // left out of the denoising argmax and softmax
+    float threshold;
+    int32_t* n_committed;                 // [batch]
+    int32_t* n_masked;                    // [batch] masks left after the commit
+    float* conf_out;                      // optional [M]
+    uint32_t* status;
 };
 
 enum PackKind { PACK_LINEAR = 0, PACK_QKV = 1, PACK_GATE_UP = 2 };

@@ -14,7 +14,8 @@ import torch
 from . import _lib as C
 
 __all__ = ["DeviceModel", "DeviceCache", "Workspace", "block_forward", "draft", "verify_accept",
-           "accept_from_logits", "read_device_status", "stream_handle", "VERIFY", "DRAFT"]
+           "accept_from_logits", "denoise_step", "refresh_block", "commit_from_logits", "read_device_status",
+           "stream_handle", "VERIFY", "DRAFT"]
 
 VERIFY = C.NLD_MODE_VERIFY
 DRAFT = C.NLD_MODE_DRAFT
@@ -211,6 +212,48 @@ def accept_from_logits(logits: torch.Tensor, drafts, device="cuda"):
     C.check(lib.nld_accept_from_logits(_ptr(logits), _ptr(drafts), batch, k, vocab, _ptr(out["argmax"]),
                                        _ptr(out["accept_len"]), _ptr(out["committed"]), _ptr(out["next_anchor"]),
                                        _ptr(ws), n, stream_handle()))
+    return out
+
+
+def denoise_step(model, cache, ws, block: torch.Tensor, threshold: float, bidir_from: int = 0, want_logits=False,
+                 outs=None):
+    """One Mode 2 denoising step; ``block`` (int32 [batch][k], device) is updated in place.
+    Returns dict of device tensors: n_committed, n_masked, confidence [batch][k], logits (or None)."""
+    batch, k = block.shape
+    dev = model.device
+    if outs is None:
+        outs = {"n_committed": torch.empty(batch, dtype=torch.int32, device=dev),
+                "n_masked": torch.empty(batch, dtype=torch.int32, device=dev),
+                "confidence": torch.empty((batch, k), dtype=torch.float32, device=dev)}
+    logits = torch.empty((batch, k, model.shape.vocab), dtype=torch.float32, device=dev) if want_logits else None
+    C.check(C.load().nld_denoise_step(model.handle, ctypes.byref(cache.struct), _ptr(block), batch, k, bidir_from,
+                                      float(threshold), _ptr(outs["n_committed"]), _ptr(outs["n_masked"]),
+                                      _ptr(outs.get("confidence")), _ptr(logits), ws.ptr, ws.nbytes, stream_handle()))
+    outs = dict(outs)
+    outs["logits"] = logits
+    return outs
+
+
+def refresh_block(model, cache, ws, block: torch.Tensor, next_anchor=None):
+    """Causal K/V refresh of completed blocks (commits k-1 rows).  Returns next_anchor (int32 [batch])."""
+    batch, k = block.shape
+    nxt = next_anchor if next_anchor is not None else torch.empty(batch, dtype=torch.int32, device=model.device)
+    C.check(C.load().nld_refresh_block(model.handle, ctypes.byref(cache.struct), _ptr(block), batch, k, _ptr(nxt),
+                                       ws.ptr, ws.nbytes, stream_handle()))
+    return nxt
+
+
+def commit_from_logits(logits: torch.Tensor, block: torch.Tensor, mask_token_id: int, threshold: float):
+    """The denoising commit from given f32 logits [batch][k][vocab]; ``block`` is updated in place."""
+    batch, k, vocab = logits.shape
+    dev = logits.device
+    out = {"argmax": torch.empty((batch, k), dtype=torch.int32, device=dev),
+           "n_committed": torch.empty(batch, dtype=torch.int32, device=dev),
+           "n_masked": torch.empty(batch, dtype=torch.int32, device=dev),
+           "confidence": torch.empty((batch, k), dtype=torch.float32, device=dev)}
+    C.check(C.load().nld_commit_from_logits(_ptr(logits), _ptr(block), batch, k, vocab, mask_token_id,
+                                            float(threshold), _ptr(out["argmax"]), _ptr(out["n_committed"]),
+                                            _ptr(out["n_masked"]), _ptr(out["confidence"]), stream_handle()))
     return out
 
 

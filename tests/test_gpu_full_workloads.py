@@ -152,3 +152,46 @@ def test_14b_self_speculation_step(R):
         assert int(cache.lengths.cpu()[b]) == int(plens[b]) + L + 1
     check_argmax(g_a[seqs], g_v[seqs], ref_v, e_v * np.max(np.abs(ref_v)))
     assert R.read_device_status(ws) == 0
+
+
+def test_8b_full_denoising_step_and_refresh(R):
+    """Mode 2 at the full 8B size (36 layers, prefix 4096, k=16): one denoising step from [anchor, masks]
+    at a threshold every confidence exceeds (the whole block is decoded at once), then the refresh of the
+    oracle's decoded block, compared on the K/V rows of every layer, the lengths and the next anchor."""
+    wl, shape, k, B, plens, max_len, model, cache, okv, w = _setup(R, "8b", [0])
+    mask = shape.mask_token_id
+    anchor = synth_tokens(shape, wl.seed, "test.8b.m2.anchor", (1,))
+    block = O.draft_block(anchor, k, mask)
+    ws = R.Workspace(model, B, k, max_len)
+    blk = torch.from_numpy(block.copy()).cuda()
+    out = R.denoise_step(model, cache, ws, blk, -1.0, want_logits=True)
+    log("8b: oracle denoising step")
+    ref = O.denoise_step(w, okv, block, -1.0)
+    g = out["logits"].cpu().numpy()
+    e = rel_err(g, ref["logits"])
+    log("8b: denoising rel err %.3e" % e)
+    assert e <= TOL
+    err_abs = e * float(np.max(np.abs(ref["logits"])))
+    g_conf = out["confidence"].cpu().numpy()
+    np.testing.assert_allclose(g_conf, O.top1_confidence(O.denoising_logits(g, mask)), rtol=1e-5)
+    assert np.all(np.abs(np.log(g_conf.astype(np.float64)) - np.log(ref["conf"])) <= 2 * err_abs + 1e-6)
+    g_block = blk.cpu().numpy()
+    own = O.argmax_first(O.denoising_logits(g, mask))
+    assert np.array_equal(g_block[:, 1:], own[:, 1:]) and g_block[0, 0] == anchor[0]
+    assert int(out["n_committed"].cpu()[0]) == k - 1 and int(out["n_masked"].cpu()[0]) == 0
+    near = check_argmax(own[:, 1:], np.where(np.arange(shape.vocab) == mask, -np.inf, g)[:, 1:],
+                        O.denoising_logits(ref["logits"], mask)[:, 1:], err_abs)
+    log("8b: near-tie denoised rows differing: %s" % near)
+    assert int(cache.lengths.cpu()[0]) == int(plens[0])          # denoising never commits
+    P = int(plens[0])
+    dec = ref["block"]
+    nxt = R.refresh_block(model, cache, ws, torch.from_numpy(dec).cuda())
+    log("8b: oracle refresh")
+    nxt_o = O.refresh(w, okv, dec)
+    assert int(nxt.cpu()[0]) == int(nxt_o[0])
+    assert int(cache.lengths.cpu()[0]) == P + k - 1 == int(okv.lengths[0])
+    for l in range(shape.n_layers):
+        kg, vg = cache.read_kv(l, P, P + k - 1)
+        assert rel_err(O.bf16_bits_to_float(kg), okv.k[l][:, :, P:P + k - 1]) < TOL, "layer %d K" % l
+        assert rel_err(O.bf16_bits_to_float(vg), okv.v[l][:, :, P:P + k - 1]) < TOL, "layer %d V" % l
+    assert R.read_device_status(ws) == 0
