@@ -19,6 +19,10 @@ What it computes (arXiv 2607.05722):
 * Mode 1 (Sec. 3.1), AR decoding, is the verify pass with a one-token block.
 * The first-mismatch index j* of the LoRA paragraph in Sec. 3.3 restates the
   acceptance rule and is the form used here.
+* The LoRA-enhanced drafter of Sec. 3.3: an adapter on the attention's O
+  projection that only the diffusion (draft-mode) passes use, the AR pathway
+  left unchanged.  Standard LoRA form: the O projection's output gains
+  (alpha / r) * B A o for rank r, A [r][q_dim], B [hidden][r].
 * Mode 2 (Sec. 3.2), block-wise diffusion denoising with confidence-based
   sampling: repeated draft passes over a block that commit masked positions by
   a confidence threshold, then a causal K/V refresh of the completed block
@@ -124,6 +128,11 @@ def block_visibility(prefix_len: int, k: int, mode: str, bidir_from: int = 0) ->
     return vis
 
 
+def lora_scale(shape) -> float:
+    """LoRA output scale alpha / r (Sec. 3.3 uses r = 128, alpha = 512)."""
+    return float(shape.lora_alpha) / float(shape.lora_rank)
+
+
 def argmax_first(logits: np.ndarray) -> np.ndarray:
     """Index of the first maximum along the last axis."""
     return np.argmax(logits, axis=-1).astype(np.int32)
@@ -224,7 +233,10 @@ def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode
                 vals = np.concatenate([kv.v[l][b, g, :p_b], vb[b, :, g]], axis=0)
                 for hq in range(g * G, (g + 1) * G):
                     o[b, :, hq] = softmax_attention(q[b, :, hq], keys, vals, vis)
-        x = x + o.reshape(B, k, s.q_dim) @ w["wo"].T
+        o2 = o.reshape(B, k, s.q_dim)
+        x = x + o2 @ w["wo"].T
+        if mode == DRAFT and "lora_a" in w:
+            x = x + lora_scale(s) * ((o2 @ w["lora_a"].T) @ w["lora_b"].T)
 
         h = rms_norm(x, w["ffn_norm"], s.rms_eps)
         act = silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)
@@ -242,12 +254,13 @@ def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode
 
 
 def full_forward(weights: OracleWeights, seq_tokens: np.ndarray, visible: np.ndarray,
-                 positions: np.ndarray | None = None) -> np.ndarray:
+                 positions: np.ndarray | None = None, lora_rows: np.ndarray | None = None) -> np.ndarray:
     """Recompute every position from tokens with an explicit attention mask (no cache).
 
-    seq_tokens: int [batch, T]; visible: bool [T, T] (row attends to column).
-    Returns logits [batch, T, vocab].  This is the plain definition the cached
-    block pass must reproduce.
+    seq_tokens: int [batch, T]; visible: bool [T, T] (row attends to column);
+    lora_rows: optional bool [T], the rows that take the draft-pathway LoRA
+    (the block rows of a draft pass).  Returns logits [batch, T, vocab].  This
+    is the plain definition the cached block pass must reproduce.
     """
     s = weights.shape
     B, T = seq_tokens.shape
@@ -266,7 +279,10 @@ def full_forward(weights: OracleWeights, seq_tokens: np.ndarray, visible: np.nda
             for hq in range(s.n_q_heads):
                 g = hq // G
                 o[b, :, hq] = softmax_attention(q[b, :, hq], kk[b, :, g], vv[b, :, g], visible)
-        x = x + o.reshape(B, T, s.q_dim) @ w["wo"].T
+        o2 = o.reshape(B, T, s.q_dim)
+        x = x + o2 @ w["wo"].T
+        if lora_rows is not None and "lora_a" in w:
+            x = x + np.asarray(lora_rows)[None, :, None] * (lora_scale(s) * ((o2 @ w["lora_a"].T) @ w["lora_b"].T))
         h = rms_norm(x, w["ffn_norm"], s.rms_eps)
         x = x + (silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)) @ w["w_down"].T
     return rms_norm(x, weights.final_norm(), s.rms_eps) @ weights.lm_head().T

@@ -43,6 +43,8 @@ class ModelShape:
     rope_base: float = 10000.0
     rms_eps: float = 1e-6
     init_std: float = 0.02
+    lora_rank: int = 0          # draft-pathway LoRA on the O projection (0: none)
+    lora_alpha: float = 0.0
 
     @property
     def mask_token_id(self) -> int:
@@ -103,9 +105,11 @@ WORKLOADS = {
 
 # ----------------------------------------------------------------------------- weights
 def layer_weights(shape: ModelShape, seed: int, layer: int) -> dict:
-    """Row-major [out][in] bf16 bit patterns of one decoder layer."""
+    """Row-major [out][in] bf16 bit patterns of one decoder layer (plus lora_a [rank][q_dim] and
+    lora_b [hidden][rank] when the shape has a LoRA rank; both N(0, init_std) so that the adapter is
+    not the identity a fresh LoRA would be)."""
     h, s, p = shape.hidden, shape.init_std, "layer%d." % layer
-    return {
+    w = {
         "attn_norm": bf16_ones(h),
         "wq": normal_bf16(seed, p + "wq", (shape.q_dim, h), s),
         "wk": normal_bf16(seed, p + "wk", (shape.kv_dim, h), s),
@@ -116,6 +120,10 @@ def layer_weights(shape: ModelShape, seed: int, layer: int) -> dict:
         "w_up": normal_bf16(seed, p + "w_up", (shape.ffn, h), s),
         "w_down": normal_bf16(seed, p + "w_down", (h, shape.ffn), s),
     }
+    if shape.lora_rank:
+        w["lora_a"] = normal_bf16(seed, p + "lora_a", (shape.lora_rank, shape.q_dim), s)
+        w["lora_b"] = normal_bf16(seed, p + "lora_b", (h, shape.lora_rank), s)
+    return w
 
 
 def embed_weights(shape: ModelShape, seed: int) -> np.ndarray:

@@ -497,3 +497,59 @@ def test_refresh_rejects_an_incomplete_block(mode2):
     kv = prefilled(w, prefix[:, :-1], capacity=64)
     with pytest.raises(ValueError):
         O.refresh(w, kv, O.draft_block(prefix[:, -1], 4, MINI.mask_token_id))
+
+
+# ----------------------------------------------------------------------------- LoRA-enhanced drafter
+MINI_LORA = ModelShape(**{**MINI.__dict__, "lora_rank": 8, "lora_alpha": 32.0})
+
+
+class _MergedLoRA(O.OracleWeights):
+    """The same model with each adapter merged into the O projection, W_o + (alpha/r) B A (float64)."""
+
+    def layer(self, l):
+        w = super().layer(l)
+        w["wo"] = w["wo"] + (self.shape.lora_alpha / self.shape.lora_rank) * (w.pop("lora_b") @ w.pop("lora_a"))
+        return w
+
+
+@pytest.fixture(scope="module")
+def lora_mini():
+    w = O.OracleWeights(MINI_LORA, LazyWeights(MINI_LORA, 11), np.float64)
+    base = mini_weights()            # same seed and names: the same base weights without the adapter
+    prefix = synth_tokens(MINI, 15, "pin.lora.prefix", (2, 12))
+    block = synth_tokens(MINI, 15, "pin.lora.block", (2, 6))
+    return w, base, prefix, block
+
+
+def test_lora_leaves_the_verify_pass_unchanged(lora_mini):
+    """The adapter belongs to the diffusion pathway only: verify logits and K/V equal the base model's."""
+    w, base, prefix, block = lora_mini
+    a = O.block_forward(w, prefilled(w, prefix), block, O.VERIFY)
+    b = O.block_forward(base, prefilled(base, prefix), block, O.VERIFY)
+    np.testing.assert_array_equal(a[0], b[0])
+    for l in range(MINI.n_layers):
+        np.testing.assert_array_equal(a[1][l], b[1][l])
+
+
+def test_lora_draft_equals_merged_weights(lora_mini):
+    """A draft pass with the adapter equals a draft pass whose O projection is W_o + (alpha/r) B A (the
+    adapter merged into the weight), and differs from the base model's draft."""
+    w, base, prefix, block = lora_mini
+    merged = _MergedLoRA(MINI_LORA, LazyWeights(MINI_LORA, 11), np.float64)
+    kv = prefilled(base, prefix)               # the prefix cache is AR-pathway: the same for all three
+    got = O.block_forward(w, kv, block, O.DRAFT)[0]
+    ref = O.block_forward(merged, kv, block, O.DRAFT)[0]
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-12)
+    assert rel(O.block_forward(base, kv, block, O.DRAFT)[0], ref) > 1e-3
+
+
+def test_lora_draft_equals_full_recompute(lora_mini):
+    """The cached draft pass with the adapter equals full recompute over [prefix; block] where only the
+    block rows take the adapter and the block is bidirectional."""
+    w, base, prefix, block = lora_mini
+    kv = prefilled(base, prefix)
+    got = O.block_forward(w, kv, block, O.DRAFT)[0]
+    P, k = prefix.shape[1], block.shape[1]
+    seq = np.concatenate([prefix, block], axis=1)
+    full = O.full_forward(w, seq, O.sequence_visibility(P, k, O.DRAFT), lora_rows=np.arange(P + k) >= P)
+    np.testing.assert_allclose(got, full[:, P:], rtol=1e-10, atol=1e-12)
