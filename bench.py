@@ -10,9 +10,10 @@ device).  The timed steps replay one captured HIP graph.
 
 value = block tokens pushed through block-decode passes per second
       = 2 passes x batch x k per step / step time.
-Also timed (reported under "mode2", not part of value): one Mode 2 denoising step
-over [anchor, mask x (k-1)] at threshold 0.9 and one K/V refresh of a completed
-block, each replayed from its own captured graph.
+Also timed (not part of value), each replayed from its own captured graph:
+"mode2" -- one Mode 2 denoising step over [anchor, mask x (k-1)] at threshold
+0.9 and one K/V refresh of a completed block; "lora_draft" -- a draft pass with
+and without the LoRA-enhanced drafter's adapter (rank 128) on the O projection.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -67,6 +68,25 @@ def refresh_bytes(shape, batch, k, prefix_lens):
         + (shape.n_layers - 1) * (kb["attention"] + kb["o_proj"] + kb["gate_up"] + kb["down"])
 
 
+def graph_ms(fn, reps):
+    """Mean ms of fn() replayed `reps` times from a captured graph (one eager call and one replay first)."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.current_stream()):
+        fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def mode2_timing(R, model, cache, ws, anchor, block_full, k, reps, threshold=0.9):
     """Mean ms of one denoising step (block reset to [anchor, masks] first) and of one refresh (lengths reset
     first, so every replay refreshes the same rows), each from a captured graph replayed `reps` times."""
@@ -90,26 +110,31 @@ def mode2_timing(R, model, cache, ws, anchor, block_full, k, reps, threshold=0.9
         cache.lengths.copy_(len0)
         R.refresh_block(model, cache, ws, block_full, next_anchor=nxt)
 
-    res = {}
-    for name, fn in (("denoise_step", denoise), ("refresh", refresh)):
-        fn()
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=torch.cuda.current_stream()):
-            fn()
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        res[name] = e0.elapsed_time(e1) / reps
+    res = {name: graph_ms(fn, reps) for name, fn in (("denoise_step", denoise), ("refresh", refresh))}
     committed = int(outs["n_committed"].sum().item())
     cache.lengths.copy_(len0)
     torch.cuda.synchronize()
     return res, committed
+
+
+LORA_RANK, LORA_ALPHA = 128, 512.0     # the adapter size of the LoRA-enhanced drafter (Sec. 3.3)
+
+
+def lora_timing(R, model, cache, ws, anchor, k, reps, wl):
+    """Mean ms of a plain draft pass and of a draft pass with a rank-128 adapter on the O projection
+    attached to the same weights (seeded adapter weights), each replayed from a captured graph."""
+    import torch
+    from synth.workloads import ModelShape, lora_weights
+    lshape = ModelShape(**{**model.shape.__dict__, "lora_rank": LORA_RANK, "lora_alpha": LORA_ALPHA})
+    lmodel = model.with_lora(lshape, lambda l: lora_weights(lshape, wl.seed, l))
+    lws = R.Workspace(lmodel, anchor.shape[0], k, cache.max_len)      # holds the adapter's intermediate too
+    B = anchor.shape[0]
+    d = torch.empty((B, k - 1), dtype=torch.int32, device=anchor.device)
+    res = {"draft": graph_ms(lambda: R.draft(model, cache, ws, anchor, k, out=d), reps),
+           "lora_draft": graph_ms(lambda: R.draft(lmodel, cache, lws, anchor, k, out=d), reps)}
+    res["status"] = R.read_device_status(lws)
+    lmodel.close()
+    return res
 
 
 def blas_threads():
@@ -294,7 +319,8 @@ def main():
 
         block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
         m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
-        status |= R.read_device_status(ws)
+        lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
+        status |= R.read_device_status(ws) | lora_ms["status"]
 
     ms_per_step = elapsed_ms / steps
     value = 2.0 * B * k / (ms_per_step * 1e-3)
@@ -348,6 +374,14 @@ def main():
                                       / HBM_PEAK_GBS, 4),
             "threshold": 0.9,
             "first_step_commits": m2_committed,
+        },
+        "lora_draft": {
+            "rank": LORA_RANK, "alpha": LORA_ALPHA,
+            "draft_pass_ms": round(lora_ms["draft"], 4),
+            "lora_draft_pass_ms": round(lora_ms["lora_draft"], 4),
+            "lora_draft_hbm_frac": round((pass_bytes(shape, B, k, plens) + shape.n_layers * 2 * LORA_RANK
+                                          * (shape.q_dim + shape.hidden)) / (lora_ms["lora_draft"] * 1e-3) / 1e9
+                                         / HBM_PEAK_GBS, 4),
         },
     }
     if not args.no_cpu_baseline:

@@ -86,6 +86,14 @@ typedef struct {
     float rope_base;
     float rms_eps;
     int32_t mask_token_id; /* token placed in draft rows 1..k-1 */
+    /* LoRA-enhanced drafter (Sec. 3.3): an adapter on the O projection used only by
+     * draft-mode passes (the draft pass, denoising steps, nld_block_forward with
+     * NLD_MODE_DRAFT); verify passes never read it.  A draft pass adds
+     * lora_scale * B (A o) to the O projection's output, A = lora_a [lora_rank][n_q_heads*head_dim],
+     * B = lora_b [hidden][lora_rank] (standard LoRA, lora_scale = alpha / rank; the paper
+     * uses rank 128, alpha 512).  lora_rank 0 (no adapter) or a multiple of 32. */
+    int32_t lora_rank;
+    float lora_scale;
 } nld_config;
 
 /* Per-layer weights.  Norm gains are plain bf16 vectors; matrices must be in
@@ -97,6 +105,8 @@ typedef struct {
     const void* ffn_norm;    /* bf16 [hidden] */
     const void* w_gate_up;   /* nld_pack_gate_up(Wg, Wu) */
     const void* w_down;      /* nld_pack_linear(Wd [hidden][ffn]) */
+    const void* lora_a;      /* nld_pack_linear(A [lora_rank][n_q_heads*head_dim]); NULL when lora_rank = 0 */
+    const void* lora_b;      /* nld_pack_linear(B [hidden][lora_rank]); NULL when lora_rank = 0 */
 } nld_layer_weights;
 
 typedef struct {
@@ -134,9 +144,11 @@ const char* nld_last_error(void);
 const char* nld_status_string(int32_t status);
 
 /* Validate `cfg` and the weight pointers (host-side only) and build a handle.
- * Errors: INVALID_ARG (null pointer, non-positive size), SHAPE (hidden not a
- * multiple of 32, head_dim not 64/128, n_q_heads not a multiple of
- * n_kv_heads, ffn not a multiple of 8).  No device call is made. */
+ * Errors: INVALID_ARG (null pointer, non-positive size, a negative or
+ * non-finite LoRA setting, missing adapter weights when lora_rank > 0), SHAPE
+ * (hidden not a multiple of 32, head_dim not 64/128, n_q_heads not a multiple
+ * of n_kv_heads, ffn not a multiple of 8, lora_rank not a multiple of 32).
+ * No device call is made. */
 nld_status nld_model_create(const nld_config* cfg, const nld_weights* w, nld_model** out);
 void nld_model_destroy(nld_model* m);
 

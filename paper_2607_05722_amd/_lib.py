@@ -42,12 +42,12 @@ TRACE_CLASSES = ["embed", "qkv", "attention", "o_proj", "gate_up", "down", "lm_h
 class Config(ctypes.Structure):
     _fields_ = [("n_layers", c_i32), ("hidden", c_i32), ("n_q_heads", c_i32), ("n_kv_heads", c_i32),
                 ("head_dim", c_i32), ("ffn", c_i32), ("vocab", c_i32), ("rope_base", c_f32),
-                ("rms_eps", c_f32), ("mask_token_id", c_i32)]
+                ("rms_eps", c_f32), ("mask_token_id", c_i32), ("lora_rank", c_i32), ("lora_scale", c_f32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [("attn_norm", c_vp), ("w_qkv", c_vp), ("w_o", c_vp), ("ffn_norm", c_vp),
-                ("w_gate_up", c_vp), ("w_down", c_vp)]
+                ("w_gate_up", c_vp), ("w_down", c_vp), ("lora_a", c_vp), ("lora_b", c_vp)]
 
 
 class Weights(ctypes.Structure):

@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, lora_t, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -126,6 +126,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
     L.blk_v = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);
+    L.lora_t = take(4 * (size_t)L.Mpad * c.lora_rank);   // split lora_scale * (A o), draft passes only
     L.total = off;
     return L;
 }
@@ -144,6 +145,9 @@ nld_status check_config(const nld_config* c) {
     if (c->mask_token_id < 0 || c->mask_token_id >= c->vocab)
         return fail(NLD_ERR_INVALID_ARG, "mask_token_id outside [0, vocab)");
     if (!(c->rope_base > 1.0f) || !(c->rms_eps >= 0.0f)) return fail(NLD_ERR_INVALID_ARG, "bad rope_base or rms_eps");
+    if (c->lora_rank < 0 || !(fabsf(c->lora_scale) < INFINITY))
+        return fail(NLD_ERR_INVALID_ARG, "lora_rank must be >= 0 and lora_scale finite");
+    if (c->lora_rank % 32) return fail(NLD_ERR_SHAPE, "lora_rank (%d) must be a multiple of 32", c->lora_rank);
     return NLD_OK;
 }
 
@@ -366,6 +370,27 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         go.W = (const uint4*)W.w_o;
         go.n_tiles = c.hidden / 16;
         go.ksteps = ks_q;
+        if (io.mode == NLD_MODE_DRAFT && c.lora_rank > 0) {
+            // LoRA down-projection t = lora_scale * (A o), split; the O projection then takes
+            // B as lora_rank / 32 more k-steps against t
+            GemmArgs gt{};
+            gt.A = at<uint16_t>(ws, L.o);
+            gt.M = M;
+            gt.K = nq * D;
+            gt.W = (const uint4*)W.lora_a;
+            gt.n_tiles = c.lora_rank / 16;
+            gt.ksteps = ks_q;
+            gt.xg_out = at<uint16_t>(ws, L.lora_t);
+            gt.out_scale = c.lora_scale;
+            {
+                TraceScope ts(NLD_TRACE_O_PROJ, s);
+                const StreamPlan p = plan_stream(EPI_SPLIT, M, gt.n_tiles);
+                HIP_TRY(launch_gemm_stream(EPI_SPLIT, p.mt, p.ct, p.nw, p.gx, p.gy, gt, s));
+            }
+            go.W2 = (const uint4*)W.lora_b;
+            go.A2 = at<uint16_t>(ws, L.lora_t);
+            go.ksteps2 = c.lora_rank / 32;
+        }
         go.x = x;
         go.xg_out = at<uint16_t>(ws, L.xg);
         go.gain_next = (const uint16_t*)W.ffn_norm;
@@ -498,6 +523,8 @@ nld_status nld_model_create(const nld_config* cfg, const nld_weights* w, nld_mod
         const nld_layer_weights& L = w->layers[l];
         if (!L.attn_norm || !L.w_qkv || !L.w_o || !L.ffn_norm || !L.w_gate_up || !L.w_down)
             return fail(NLD_ERR_INVALID_ARG, "a weight pointer of layer %d is NULL", l);
+        if (cfg->lora_rank > 0 && (!L.lora_a || !L.lora_b))
+            return fail(NLD_ERR_INVALID_ARG, "lora_rank > 0 but layer %d has no lora_a/lora_b", l);
     }
     nld_model* m = new nld_model;
     m->cfg = *cfg;

@@ -347,9 +347,10 @@ struct Batch {
     uint4 xl[SPLIT ? U : 1][SPLIT ? MT : 1];
 };
 
-template <int MT, int CT, int NW, int EPI>
+template <int MT, int CT, int NW, int EPI, bool XK>
 __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     constexpr bool SPLIT = true;
+    constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LMHEAD;
     typedef Batch<MT, CT, SPLIT> B;
     constexpr int U = B::U;
     constexpr int BSTRIDE = SPLIT ? 1024 : 512;   // elements per (row tile, k-step) block
@@ -364,9 +365,11 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     const int t0 = blockIdx.x * CT;
     const int m0 = blockIdx.y * 16 * MT;
 
-    const int per = (a.ksteps + NW - 1) / NW;
-    const int s_begin = min(a.ksteps, wave * per);
-    const int s_end = min(a.ksteps, s_begin + per);
+    // k-steps [0, ksteps) come from (W, A); with XK, [ksteps, ksteps + ksteps2) from (W2, A2)
+    const int KT = XK ? a.ksteps + a.ksteps2 : a.ksteps;
+    const int per = (KT + NW - 1) / NW;
+    const int s_begin = min(KT, wave * per);
+    const int s_end = min(KT, s_begin + per);
 
     const uint4* wp[CT];
 #pragma unroll
@@ -380,6 +383,18 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     for (int mt = 0; mt < MT; ++mt) {
         aok[mt] = m0 + mt * 16 + r < a.M;
         ap[mt] = a.A + (size_t)(blockIdx.y * MT + mt) * a.ksteps * BSTRIDE + (size_t)lane * 8;
+    }
+    const uint4* wp2[CT];
+    const uint16_t* ap2[MT];
+    if constexpr (XK) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            const int t = min(t0 + ct, a.n_tiles - 1);
+            wp2[ct] = a.W2 + (size_t)t * a.ksteps2 * 64 + lane;
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            ap2[mt] = a.A2 + (size_t)(blockIdx.y * MT + mt) * a.ksteps2 * BSTRIDE + (size_t)lane * 8;
     }
 
     f32x4_t acc[MT][CT], accl[SPLIT ? MT : 1][SPLIT ? CT : 1];
@@ -419,14 +434,21 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         for (int u = 0; u < U; ++u) {
             const int ss = s + u;
             const bool in = ss < s_end;
+            // second source: wave-uniform; its columns are whole k-steps, never past its end
+            const bool second = XK && ss >= a.ksteps;
+            const int s2 = ss - a.ksteps;
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) buf.w[u][ct] = in ? wp[ct][(size_t)ss * 64] : zero4;
+            for (int ct = 0; ct < CT; ++ct) {
+                const uint4* src = second ? wp2[ct] + (size_t)s2 * 64 : wp[ct] + (size_t)ss * 64;
+                buf.w[u][ct] = in ? *src : zero4;
+            }
             const int kcol = ss * 32 + 8 * g;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const bool ok = in && aok[mt] && kcol < a.K;
-                buf.x[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE) : zero4;
-                if constexpr (SPLIT) buf.xl[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE + SPLIT_LO) : zero4;
+                const bool ok = in && aok[mt] && (second || kcol < a.K);
+                const uint16_t* asrc = second ? ap2[mt] + (size_t)s2 * BSTRIDE : ap[mt] + (size_t)ss * BSTRIDE;
+                buf.x[u][mt] = ok ? *(const uint4*)asrc : zero4;
+                if constexpr (SPLIT) buf.xl[u][mt] = ok ? *(const uint4*)(asrc + SPLIT_LO) : zero4;
             }
         }
     };
@@ -444,7 +466,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
 
     B b0, b1;
     load(s_begin, b0);
-    if constexpr (EPI != EPI_RESID) rms_scales(a, m0, 16 * MT, inv_s);   // visible after the barrier below
+    if constexpr (NORMED) rms_scales(a, m0, 16 * MT, inv_s);   // visible after the barrier below
     for (int s = s_begin; s < s_end; s += 2 * U) {
         load(s + U, b1);
         compute(b0);
@@ -490,6 +512,8 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
             epi_qkv(a, v * inv_s[ml], m, t, lane, pos);
         } else if constexpr (EPI == EPI_SWIGLU) {
             epi_swiglu(a, v * inv_s[ml], m, t, lane);
+        } else if constexpr (EPI == EPI_SPLIT) {
+            if (m < a.M) store_split(a.xg_out, split_index(m, t * 16 + r, a.n_tiles / 2), a.out_scale * v);
         } else {
             float2 tl;
             const unsigned long long key = epi_lmhead(a, v * inv_s[ml], m, t, lane, &tl);
@@ -516,22 +540,22 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     }
 }
 
-template <int EPI, int MT>
+template <int EPI, int MT, bool XK>
 static hipError_t launch_stream_ct(int ct, int nw, dim3 grid, const GemmArgs& a, hipStream_t s) {
-    if (ct == 1 && nw == 8) gemm_stream_kernel<MT, 1, 8, EPI><<<grid, 512, 0, s>>>(a);
-    else if (ct == 2 && nw == 8) gemm_stream_kernel<MT, 2, 8, EPI><<<grid, 512, 0, s>>>(a);
-    else if (ct == 4 && nw == 4) gemm_stream_kernel<MT, 4, 4, EPI><<<grid, 256, 0, s>>>(a);
-    else if (ct == 1 && nw == 4) gemm_stream_kernel<MT, 1, 4, EPI><<<grid, 256, 0, s>>>(a);
+    if (ct == 1 && nw == 8) gemm_stream_kernel<MT, 1, 8, EPI, XK><<<grid, 512, 0, s>>>(a);
+    else if (ct == 2 && nw == 8) gemm_stream_kernel<MT, 2, 8, EPI, XK><<<grid, 512, 0, s>>>(a);
+    else if (ct == 4 && nw == 4) gemm_stream_kernel<MT, 4, 4, EPI, XK><<<grid, 256, 0, s>>>(a);
+    else if (ct == 1 && nw == 4) gemm_stream_kernel<MT, 1, 4, EPI, XK><<<grid, 256, 0, s>>>(a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
-template <int EPI>
+template <int EPI, bool XK = false>
 static hipError_t launch_stream_mt(int mt, int ct, int nw, dim3 grid, const GemmArgs& a, hipStream_t s) {
     switch (mt) {
-        case 1: return launch_stream_ct<EPI, 1>(ct, nw, grid, a, s);
-        case 2: return launch_stream_ct<EPI, 2>(ct, nw, grid, a, s);
-        case 4: return launch_stream_ct<EPI, 4>(ct, nw, grid, a, s);
+        case 1: return launch_stream_ct<EPI, 1, XK>(ct, nw, grid, a, s);
+        case 2: return launch_stream_ct<EPI, 2, XK>(ct, nw, grid, a, s);
+        case 4: return launch_stream_ct<EPI, 4, XK>(ct, nw, grid, a, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -539,11 +563,15 @@ static hipError_t launch_stream_mt(int mt, int ct, int nw, dim3 grid, const Gemm
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s) {
     const dim3 grid(grid_x, grid_y);
+    if (a.W2 && epi != EPI_RESID) return hipErrorInvalidValue;
     switch (epi) {
         case EPI_QKV: return launch_stream_mt<EPI_QKV>(mt, ct, nw, grid, a, s);
-        case EPI_RESID: return launch_stream_mt<EPI_RESID>(mt, ct, nw, grid, a, s);
+        case EPI_RESID:
+            return a.W2 ? launch_stream_mt<EPI_RESID, true>(mt, ct, nw, grid, a, s)
+                        : launch_stream_mt<EPI_RESID>(mt, ct, nw, grid, a, s);
         case EPI_SWIGLU: return launch_stream_mt<EPI_SWIGLU>(mt, ct, nw, grid, a, s);
         case EPI_LMHEAD: return launch_stream_mt<EPI_LMHEAD>(mt, ct, nw, grid, a, s);
+        case EPI_SPLIT: return launch_stream_mt<EPI_SPLIT>(mt, ct, nw, grid, a, s);
         default: return hipErrorInvalidValue;
     }
 }

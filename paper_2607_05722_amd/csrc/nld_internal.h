@@ -77,7 +77,7 @@ __device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
 }
 
 // ---------------------------------------------------------------- kernel arguments
-enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
+enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3, EPI_SPLIT = 4 };
 
 struct GemmArgs {
     // A operand: split bf16 activations in operand order (split_index with `ksteps`).
@@ -95,6 +95,14 @@ struct GemmArgs {
     int n_tiles;
     int ksteps;          // ceil(K / 32)
     unsigned* tile_ctr;  // normed GEMM: dynamic tile counter (zeroed by the embedding kernel each pass)
+    // Second reduction source (streamed GEMM only): k-steps [ksteps, ksteps + ksteps2)
+    // read W2 (packed, ksteps2 steps per tile) against A2 (split, ksteps2 steps per row
+    // tile).  The draft pass's O projection uses it for the LoRA up-projection.
+    const uint4* W2;
+    const uint16_t* A2;
+    int ksteps2;
+    // EPI_SPLIT: xg_out gets the split operand out_scale * (A W^T) (split_index with n_tiles/2 steps)
+    float out_scale;
     // EPI_RESID: x += A W^T, then the next RMSNorm's operand and statistics
     float* x;
     uint16_t* xg_out;          // split x * gain_next, split_index with N/32 steps
@@ -219,6 +227,7 @@ int gemm_norm_max_waves(int ks);
 hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs& a, hipStream_t s);
 // Streamed GEMM: 16*mt rows x 16*ct columns per workgroup, nw wavefronts split K.
 // normed: the operand is an RMSNorm output (per-row scale from part_ss).
+// With a.W2 set (EPI_RESID only) the reduction continues over the second source.
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
 // kh: key halves per stage (2 when the unit has at most 4 row tiles, else 1); 8 wavefronts per workgroup.

@@ -36,8 +36,21 @@ def _ptr(t) -> int:
 
 
 def make_config(shape) -> C.Config:
+    rank = int(getattr(shape, "lora_rank", 0))
+    scale = float(shape.lora_alpha) / rank if rank else 0.0
     return C.Config(shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
-                    shape.vocab, float(shape.rope_base), float(shape.rms_eps), int(shape.mask_token_id))
+                    shape.vocab, float(shape.rope_base), float(shape.rms_eps), int(shape.mask_token_id), rank, scale)
+
+
+def _pack_lora(lib, shape, rank, device, w, packed, s):
+    """Pack one layer's adapter: lora_a [rank][q_dim] and lora_b [hidden][rank] (row-major bits)."""
+    qd, h = shape.q_dim, shape.hidden
+    a, b = _bits_to_device(w["lora_a"], device), _bits_to_device(w["lora_b"], device)
+    la, lb = packed(C.NLD_PACK_LINEAR, rank, qd), packed(C.NLD_PACK_LINEAR, h, rank)
+    C.check(lib.nld_pack_linear(_ptr(a), rank, qd, _ptr(la), s))
+    C.check(lib.nld_pack_linear(_ptr(b), h, rank, _ptr(lb), s))
+    torch.cuda.current_stream().synchronize()
+    return la, lb
 
 
 class DeviceModel:
@@ -80,9 +93,12 @@ class DeviceModel:
             wd = _bits_to_device(w["w_down"], self.device)
             dn = packed(C.NLD_PACK_LINEAR, h, f)
             C.check(self.lib.nld_pack_linear(_ptr(wd), h, f, _ptr(dn), s))
+            la = lb = None
+            if self.cfg.lora_rank:
+                la, lb = self._pack_lora(w, packed, s)
             torch.cuda.current_stream().synchronize()     # row-major sources are freed below
             del wq, wk, wv, wo, wg, wu, wd
-            layers[l] = C.LayerWeights(_ptr(an), _ptr(qkv), _ptr(o), _ptr(fn), _ptr(gu), _ptr(dn))
+            layers[l] = C.LayerWeights(_ptr(an), _ptr(qkv), _ptr(o), _ptr(fn), _ptr(gu), _ptr(dn), _ptr(la), _ptr(lb))
         self.embed = _bits_to_device(source.embed, self.device)
         self.final_norm = _bits_to_device(source.final_norm, self.device)
         lm = _bits_to_device(source.lm_head, self.device)
@@ -92,6 +108,59 @@ class DeviceModel:
         del lm
         self._keep, self._layers = keep, layers
         self.weights = C.Weights(_ptr(self.embed), _ptr(self.final_norm), _ptr(self.lm_head), layers)
+        handle = ctypes.c_void_p()
+        C.check(self.lib.nld_model_create(ctypes.byref(self.cfg), ctypes.byref(self.weights), ctypes.byref(handle)))
+        self.handle = handle
+
+    def _pack_lora(self, w, packed, s):
+        return _pack_lora(self.lib, self.shape, self.cfg.lora_rank, self.device, w, packed, s)
+
+    def with_lora(self, lora_shape, lora_layer):
+        """A second handle over these weights with a draft-pathway adapter attached.  lora_shape: this
+        model's shape with lora_rank / lora_alpha set; lora_layer(l) -> dict with lora_a, lora_b bits."""
+        view = ModelView(self, lora_shape)
+        keep = []
+
+        def packed(kind, out_dim, in_dim):
+            n = self.lib.nld_packed_bytes(kind, ctypes.byref(view.cfg), out_dim, in_dim)
+            t = torch.empty(n, dtype=torch.uint8, device=self.device)
+            keep.append(t)
+            return t
+
+        s = stream_handle()
+        layers = (C.LayerWeights * self.shape.n_layers)()
+        for l in range(self.shape.n_layers):
+            base = self._layers[l]
+            la, lb = _pack_lora(self.lib, lora_shape, view.cfg.lora_rank, self.device, lora_layer(l), packed, s)
+            layers[l] = C.LayerWeights(base.attn_norm, base.w_qkv, base.w_o, base.ffn_norm, base.w_gate_up,
+                                       base.w_down, _ptr(la), _ptr(lb))
+        view.finish(layers, keep)
+        return view
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.nld_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class ModelView:
+    """A model handle that borrows a DeviceModel's weights (see DeviceModel.with_lora)."""
+
+    def __init__(self, base: DeviceModel, shape):
+        self.base, self.shape, self.device, self.lib = base, shape, base.device, base.lib
+        self.cfg = make_config(shape)
+        self.handle = None
+
+    def finish(self, layers, keep):
+        self._layers, self._keep = layers, keep
+        b = self.base
+        self.weights = C.Weights(_ptr(b.embed), _ptr(b.final_norm), _ptr(b.lm_head), layers)
         handle = ctypes.c_void_p()
         C.check(self.lib.nld_model_create(ctypes.byref(self.cfg), ctypes.byref(self.weights), ctypes.byref(handle)))
         self.handle = handle

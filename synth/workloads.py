@@ -121,9 +121,15 @@ def layer_weights(shape: ModelShape, seed: int, layer: int) -> dict:
         "w_down": normal_bf16(seed, p + "w_down", (h, shape.ffn), s),
     }
     if shape.lora_rank:
-        w["lora_a"] = normal_bf16(seed, p + "lora_a", (shape.lora_rank, shape.q_dim), s)
-        w["lora_b"] = normal_bf16(seed, p + "lora_b", (h, shape.lora_rank), s)
+        w.update(lora_weights(shape, seed, layer))
     return w
+
+
+def lora_weights(shape: ModelShape, seed: int, layer: int) -> dict:
+    """The draft-pathway adapter of one layer alone: lora_a [rank][q_dim], lora_b [hidden][rank]."""
+    p, s = "layer%d." % layer, shape.init_std
+    return {"lora_a": normal_bf16(seed, p + "lora_a", (shape.lora_rank, shape.q_dim), s),
+            "lora_b": normal_bf16(seed, p + "lora_b", (shape.hidden, shape.lora_rank), s)}
 
 
 def embed_weights(shape: ModelShape, seed: int) -> np.ndarray:

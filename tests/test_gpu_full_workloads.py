@@ -195,3 +195,33 @@ def test_8b_full_denoising_step_and_refresh(R):
         assert rel_err(O.bf16_bits_to_float(kg), okv.k[l][:, :, P:P + k - 1]) < TOL, "layer %d K" % l
         assert rel_err(O.bf16_bits_to_float(vg), okv.v[l][:, :, P:P + k - 1]) < TOL, "layer %d V" % l
     assert R.read_device_status(ws) == 0
+
+
+def test_8b_full_lora_draft(R):
+    """The 36-layer 8B draft pass with the paper's adapter (rank 128, alpha 512) attached to the benchmark's
+    weights, against the oracle with the same adapter."""
+    from synth.workloads import lora_weights
+    wl, shape, k, B, plens, max_len, model, cache, okv, _ = _setup(R, "8b", [0])
+    lshape = ModelShape(**{**shape.__dict__, "lora_rank": 128, "lora_alpha": 512.0})
+    src = LazyWeights(shape, wl.seed, keep=False)
+
+    class Src:
+        embed, lm_head, final_norm = src.embed, src.lm_head, src.final_norm
+
+        @staticmethod
+        def layer(l):
+            return {**src.layer(l), **lora_weights(lshape, wl.seed, l)}
+
+    lmodel = model.with_lora(lshape, lambda l: lora_weights(lshape, wl.seed, l))
+    anchor = synth_tokens(shape, wl.seed, "test.8b.lora.anchor", (1,))
+    ws = R.Workspace(lmodel, B, k, max_len)
+    d, dl = R.draft(lmodel, cache, ws, torch.from_numpy(anchor).cuda(), k, want_logits=True)
+    log("8b: oracle draft pass with the adapter")
+    od, ref = O.draft_pass(O.OracleWeights(lshape, Src, np.float32), okv, anchor, k)
+    g = dl.cpu().numpy()
+    e = rel_err(g, ref)
+    log("8b lora: draft rel err %.3e" % e)
+    assert e <= TOL
+    near = check_argmax(d.cpu().numpy(), g[:, 1:], ref[:, 1:], e * np.max(np.abs(ref)))
+    log("8b lora: near-tie draft rows differing: %s" % near)
+    assert R.read_device_status(ws) == 0
