@@ -229,6 +229,30 @@ nld_status nld_accept_from_logits(const float* logits, const int32_t* draft, int
                                   int32_t vocab, int32_t* argmax, int32_t* accept_len, int32_t* committed,
                                   int32_t* next_anchor, void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- a decoding loop on the device ---------------------------------------------
+ * n_steps decoding steps enqueued back to back with no host synchronisation (the
+ * sequence can be captured into a graph and replayed): with k >= 2 each step is
+ * linear self-speculation, nld_draft then nld_verify_accept (Sec. 3.3); with
+ * k = 1 each step is one AR decoding step (Sec. 3.1).  anchor [batch] is
+ * read by each step and overwritten with its next anchor; step s writes
+ * accept_len[s][batch] and committed[s][batch][k] as nld_verify_accept does, and
+ * every step advances lengths.  The drafts live in the workspace.  The cache
+ * needs room for n_steps * k more rows per sequence (else NLD_DEV_CAPACITY).
+ * Errors as nld_block_forward, plus INVALID_ARG for n_steps < 1 or a NULL
+ * anchor/accept_len/committed. */
+nld_status nld_decode_steps(const nld_model* m, const nld_kv_cache* kv, int32_t* anchor, int32_t batch, int32_t k,
+                            int32_t n_steps, int32_t bidir_from, int32_t* accept_len, int32_t* committed,
+                            void* workspace, size_t ws_bytes, void* stream);
+
+/* Host-only choice between AR decoding and self-speculation for the next steps
+ * (AR is the mode for high concurrency, Sec. 3.1, where a self-speculation step
+ * stops paying for its second pass): returns k_ss when expected_committed
+ * tokens per self-speculation step of ss_step_ms beat one token per AR step of
+ * ar_step_ms, else 1.  The caller measures both step times at its batch size
+ * and tracks expected_committed (the mean of L+1 over recent steps).  Returns 1
+ * for non-positive times or k_ss < 2. */
+int32_t nld_choose_block(float ar_step_ms, float ss_step_ms, float expected_committed, int32_t k_ss);
+
 /* ---- Mode 2: block-wise diffusion denoising (Sec. 3.2) -----------------------
  * Confidence-based decoding of one block per sequence: the block starts as
  * [anchor, mask x (k-1)] and each denoising step, one diffusion (draft) pass

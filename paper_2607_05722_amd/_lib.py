@@ -33,6 +33,7 @@ EXPORTED = [
     "nld_pack_linear", "nld_pack_qkv", "nld_pack_gate_up", "nld_workspace_bytes", "nld_workspace_init",
     "nld_block_forward", "nld_draft", "nld_verify_accept", "nld_accept_workspace_bytes",
     "nld_accept_from_logits", "nld_denoise_step", "nld_refresh_block", "nld_commit_from_logits",
+    "nld_decode_steps", "nld_choose_block",
     "nld_read_device_status", "nld_trace_enable", "nld_trace_read",
 ]
 
@@ -123,6 +124,10 @@ def load():
     L.nld_refresh_block.argtypes = [c_vp, P(KVCache), c_vp, c_i32, c_i32, c_vp, c_vp, c_sz, c_vp]
     L.nld_commit_from_logits.restype = c_i32
     L.nld_commit_from_logits.argtypes = [c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp]
+    L.nld_decode_steps.restype = c_i32
+    L.nld_decode_steps.argtypes = [c_vp, P(KVCache), c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.nld_choose_block.restype = c_i32
+    L.nld_choose_block.argtypes = [c_f32, c_f32, c_f32, c_i32]
     L.nld_read_device_status.restype = c_i32
     L.nld_read_device_status.argtypes = [c_vp, P(c_u32), c_vp]
     L.nld_trace_enable.restype = c_i32

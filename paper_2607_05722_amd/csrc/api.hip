@@ -77,7 +77,7 @@ int env_int(const char* name, int dflt) {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, lora_t, total;
+    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, lora_t, drafts, total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -127,6 +127,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
     L.blk_v = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);
     L.lora_t = take(4 * (size_t)L.Mpad * c.lora_rank);   // split lora_scale * (A o), draft passes only
+    L.drafts = take(4 * (size_t)batch * k);              // nld_decode_steps: one step's drafts
     L.total = off;
     return L;
 }
@@ -746,6 +747,51 @@ nld_status nld_commit_from_logits(const float* logits, int32_t* block, int32_t b
     fa.conf_out = confidence;
     HIP_TRY(launch_finish(fa, (hipStream_t)stream));
     return NLD_OK;
+}
+
+nld_status nld_decode_steps(const nld_model* m, const nld_kv_cache* kv, int32_t* anchor, int32_t batch, int32_t k,
+                            int32_t n_steps, int32_t bidir_from, int32_t* accept_len, int32_t* committed,
+                            void* workspace, size_t ws_bytes, void* stream) {
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, workspace, ws_bytes, &L);
+    if (st != NLD_OK) return st;
+    if (n_steps < 1) return fail(NLD_ERR_INVALID_ARG, "n_steps must be >= 1");
+    if (!anchor || !accept_len || !committed) return fail(NLD_ERR_INVALID_ARG, "anchor, accept_len or committed is NULL");
+    if (bidir_from < 0 || bidir_from > k) return fail(NLD_ERR_INVALID_ARG, "bidir_from must be in [0, k]");
+    int32_t* drafts = at<int32_t>(workspace, L.drafts);
+    hipStream_t s = (hipStream_t)stream;
+    for (int step = 0; step < n_steps; ++step) {
+        if (k >= 2) {
+            PassIO d{};
+            d.source = SRC_DRAFT;
+            d.anchor = anchor;
+            d.mode = NLD_MODE_DRAFT;
+            d.bidir_from = bidir_from;
+            d.finish = FINISH_DRAFT;
+            d.draft_out = drafts;
+            st = run_pass(m, kv, batch, k, d, workspace, L, s);
+            if (st != NLD_OK) return st;
+        }
+        PassIO v{};
+        v.source = SRC_VERIFY;
+        v.anchor = anchor;
+        v.draft_in = drafts;
+        v.mode = NLD_MODE_VERIFY;
+        v.finish = FINISH_ACCEPT;
+        v.accept_len = accept_len + (size_t)step * batch;
+        v.committed = committed + (size_t)step * batch * k;
+        v.next_anchor = anchor;   // written last by the finish kernel: the next step's anchor
+        v.advance_lengths = true;
+        st = run_pass(m, kv, batch, k, v, workspace, L, s);
+        if (st != NLD_OK) return st;
+    }
+    return NLD_OK;
+}
+
+int32_t nld_choose_block(float ar_step_ms, float ss_step_ms, float expected_committed, int32_t k_ss) {
+    if (!(ar_step_ms > 0.f) || !(ss_step_ms > 0.f) || k_ss < 2) return 1;
+    // committed tokens per millisecond: 1 per AR step, expected_committed per self-speculation step
+    return expected_committed / ss_step_ms > 1.0f / ar_step_ms ? k_ss : 1;
 }
 
 size_t nld_accept_workspace_bytes(int32_t batch, int32_t k) {

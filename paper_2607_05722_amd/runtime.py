@@ -326,6 +326,24 @@ def commit_from_logits(logits: torch.Tensor, block: torch.Tensor, mask_token_id:
     return out
 
 
+def decode_steps(model, cache, ws, anchor: torch.Tensor, k: int, n_steps: int, bidir_from: int = 0, outs=None):
+    """n_steps decoding steps on the device (self-speculation for k >= 2, AR for k = 1); ``anchor`` is
+    updated in place.  Returns dict: accept_len [n_steps][batch], committed [n_steps][batch][k]."""
+    batch = anchor.shape[0]
+    dev = model.device
+    if outs is None:
+        outs = {"accept_len": torch.empty((n_steps, batch), dtype=torch.int32, device=dev),
+                "committed": torch.empty((n_steps, batch, k), dtype=torch.int32, device=dev)}
+    C.check(C.load().nld_decode_steps(model.handle, ctypes.byref(cache.struct), _ptr(anchor), batch, k, n_steps,
+                                      bidir_from, _ptr(outs["accept_len"]), _ptr(outs["committed"]), ws.ptr,
+                                      ws.nbytes, stream_handle()))
+    return outs
+
+
+def choose_block(ar_step_ms: float, ss_step_ms: float, expected_committed: float, k_ss: int) -> int:
+    return int(C.load().nld_choose_block(ar_step_ms, ss_step_ms, expected_committed, k_ss))
+
+
 def read_device_status(ws) -> int:
     bits = ctypes.c_uint32(0)
     st = C.load().nld_read_device_status(ws.ptr, ctypes.byref(bits), stream_handle())

@@ -139,3 +139,53 @@ def test_draft_and_verify_validation():
     assert lib.nld_accept_from_logits(p, None, 1, 8, 100, p, p, p, p, p, 4096, None) == C.NLD_ERR_INVALID_ARG
     assert lib.nld_pack_linear(p, 16, 20, p, None) == C.NLD_ERR_SHAPE
     lib.nld_model_destroy(h)
+
+
+def test_lora_config_validation():
+    lib = C.load()
+    assert fake_model(lora_rank=48, lora_scale=4.0)[0] == C.NLD_ERR_SHAPE
+    assert fake_model(lora_rank=-32, lora_scale=4.0)[0] == C.NLD_ERR_INVALID_ARG
+    assert fake_model(lora_rank=32, lora_scale=float("inf"))[0] == C.NLD_ERR_INVALID_ARG
+    # a rank without adapter weights (fake_model leaves lora_a / lora_b NULL)
+    assert fake_model(lora_rank=32, lora_scale=4.0)[0] == C.NLD_ERR_INVALID_ARG
+    assert b"lora" in lib.nld_last_error()
+
+
+def test_mode2_and_decode_loop_validation():
+    lib = C.load()
+    st, h, c = fake_model()
+    kv = C.KVCache(0x1000, 0x1000, 0x1000, 1, 256)
+    need = lib.nld_workspace_bytes(h, 1, 8, 256)
+    p = 0x1000
+    nan = float("nan")
+    # denoising step: k >= 2, non-NULL block/outputs, threshold not NaN, bidir_from range, workspace size
+    assert lib.nld_denoise_step(h, ctypes.byref(kv), p, 1, 1, 0, 0.9, p, p, None, None, p, need, None) == \
+        C.NLD_ERR_INVALID_ARG
+    assert lib.nld_denoise_step(h, ctypes.byref(kv), None, 1, 8, 0, 0.9, p, p, None, None, p, need, None) == \
+        C.NLD_ERR_INVALID_ARG
+    assert lib.nld_denoise_step(h, ctypes.byref(kv), p, 1, 8, 0, nan, p, p, None, None, p, need, None) == \
+        C.NLD_ERR_INVALID_ARG
+    assert lib.nld_denoise_step(h, ctypes.byref(kv), p, 1, 8, 9, 0.9, p, p, None, None, p, need, None) == \
+        C.NLD_ERR_INVALID_ARG
+    assert lib.nld_denoise_step(h, ctypes.byref(kv), p, 1, 8, 0, 0.9, p, p, None, None, p, 64, None) == \
+        C.NLD_ERR_CAPACITY
+    assert lib.nld_refresh_block(h, ctypes.byref(kv), p, 1, 1, p, p, need, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_refresh_block(h, ctypes.byref(kv), p, 1, 8, None, p, need, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_commit_from_logits(p, p, 1, 8, 1, 0, 0.9, None, p, p, None, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_commit_from_logits(p, p, 1, 8, 100, 100, 0.9, None, p, p, None, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_commit_from_logits(p, p, 1, 8, 100, 99, nan, None, p, p, None, None) == C.NLD_ERR_INVALID_ARG
+    # decode loop
+    assert lib.nld_decode_steps(h, ctypes.byref(kv), p, 1, 8, 0, 0, p, p, p, need, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_decode_steps(h, ctypes.byref(kv), None, 1, 8, 2, 0, p, p, p, need, None) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_decode_steps(h, ctypes.byref(kv), p, 1, 8, 2, 0, p, p, p, 64, None) == C.NLD_ERR_CAPACITY
+    lib.nld_model_destroy(h)
+
+
+def test_choose_block_rule():
+    """Self-speculation wins when its expected committed tokens per ms beat one token per AR step."""
+    lib = C.load()
+    assert lib.nld_choose_block(1.0, 2.0, 3.0, 16) == 16        # 1.5 tokens/ms > 1 token/ms
+    assert lib.nld_choose_block(1.0, 2.0, 1.5, 16) == 1         # 0.75 < 1
+    assert lib.nld_choose_block(1.0, 2.0, 2.0, 16) == 1         # a tie keeps AR
+    assert lib.nld_choose_block(0.0, 2.0, 9.0, 16) == 1
+    assert lib.nld_choose_block(1.0, 2.0, 9.0, 1) == 1

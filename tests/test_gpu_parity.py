@@ -226,6 +226,62 @@ def test_tiny_planted_drafts_full_accept(R, tiny):
     assert rel_err(O.bf16_bits_to_float(kg), okv.k[0][:, :, :128 + k]) < TOL
 
 
+def _tiny_cache_copy(R, t):
+    cache = R.DeviceCache(t["shape"], 1, 256)
+    cache.k.copy_(t["cache"].k)
+    cache.v.copy_(t["cache"].v)
+    cache.lengths.copy_(t["cache"].lengths)
+    return cache
+
+
+def test_tiny_decode_steps_equal_single_calls(R, tiny):
+    """nld_decode_steps (n steps enqueued at once, anchor updated in place) equals n draft + verify_accept
+    call pairs bit for bit: accept lengths, committed tokens, anchors, lengths and cache rows."""
+    t = tiny
+    k, n = 8, 3
+    anchor = synth_tokens(t["shape"], 0, "tiny.anchor", (1,))
+    ca, cb = _tiny_cache_copy(R, t), _tiny_cache_copy(R, t)
+    wa, wb = R.Workspace(t["model"], 1, k, 256), R.Workspace(t["model"], 1, k, 256)
+    a_a, a_b = torch.from_numpy(anchor.copy()).cuda(), torch.from_numpy(anchor.copy()).cuda()
+    outs = R.decode_steps(t["model"], ca, wa, a_a, k, n)
+    acc, com = [], []
+    for _ in range(n):
+        d, _ = R.draft(t["model"], cb, wb, a_b, k)
+        o = R.verify_accept(t["model"], cb, wb, a_b, d, k, outs={
+            "accept_len": torch.empty(1, dtype=torch.int32, device="cuda"),
+            "committed": torch.empty((1, k), dtype=torch.int32, device="cuda"), "next_anchor": a_b})
+        acc.append(o["accept_len"].clone())
+        com.append(o["committed"].clone())
+    assert torch.equal(outs["accept_len"], torch.stack(acc))
+    assert torch.equal(outs["committed"], torch.stack(com))
+    assert torch.equal(a_a, a_b) and torch.equal(ca.lengths, cb.lengths)
+    end = int(ca.lengths.cpu()[0])
+    assert end >= 128 + n
+    for l in range(t["shape"].n_layers):
+        assert all(np.array_equal(x, y) for x, y in zip(ca.read_kv(l, 0, end), cb.read_kv(l, 0, end)))
+    assert R.read_device_status(wa) == 0
+
+
+def test_tiny_decode_steps_ar_mode(R, tiny):
+    """With k = 1 the loop is AR decoding: the committed tokens are the oracle's greedy continuation."""
+    t = tiny
+    n = 5
+    okv = t["okv"].copy()
+    tok = synth_tokens(t["shape"], 0, "tiny.anchor", (1,))
+    greedy = []
+    for _ in range(n):
+        tok, _ = O.ar_step(t["w"], okv, tok)
+        greedy.append(int(tok[0]))
+    cache = _tiny_cache_copy(R, t)
+    ws = R.Workspace(t["model"], 1, 1, 256)
+    a = torch.from_numpy(synth_tokens(t["shape"], 0, "tiny.anchor", (1,))).cuda()
+    outs = R.decode_steps(t["model"], cache, ws, a, 1, n)
+    assert outs["committed"][:, 0, 0].cpu().tolist() == greedy
+    assert np.all(outs["accept_len"].cpu().numpy() == 0)
+    assert int(a.cpu()[0]) == greedy[-1] and int(cache.lengths.cpu()[0]) == 128 + n
+    assert R.read_device_status(ws) == 0
+
+
 def test_capacity_error_is_reported_not_written(R, tiny):
     """A block that would run past max_len sets the capacity bit; no row beyond the cache is written."""
     t = tiny
