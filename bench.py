@@ -304,7 +304,7 @@ def main():
         committed = int((cache.lengths - len0).sum().item())
         status = R.read_device_status(ws)
 
-        # per-kernel durations, HIP events on this stream around every launch of a few eager steps
+        # per-kernel durations: every launch of a few eager steps records HIP events on its own dispatch
         lib = C.load()
         lib.nld_trace_enable(1)
         trace_steps = 3

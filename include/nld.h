@@ -301,12 +301,15 @@ nld_status nld_commit_from_logits(const float* logits, int32_t* block, int32_t b
                                   int32_t* n_masked, float* confidence, void* stream);
 
 /* ---- tracing aid -------------------------------------------------------------
- * While enabled, every kernel launch made by the block-decode calls is
- * bracketed by HIP events recorded on the call's stream (do not enable it
- * while a stream is being captured into a graph).  nld_trace_read
- * synchronizes on those events and returns, per kernel class, the summed
- * milliseconds and the launch count since the last read (host arrays of
- * length n >= NLD_TRACE_CLASSES), then clears the record. */
+ * While enabled, every kernel launch made by the block-decode calls records a
+ * pair of HIP events on its own dispatch (hipExtLaunchKernel), so the times are
+ * those of the kernels themselves, without launch gaps (do not enable it while
+ * a stream is being captured into a graph).  nld_trace_read synchronizes on
+ * those events and returns, per kernel class, the summed milliseconds and the
+ * number of class instances since the last read (host arrays of length n >=
+ * NLD_TRACE_CLASSES), then clears the record.  An instance is one step of the
+ * pass: the attention class holds the attention and merge kernels, the O
+ * projection class also the LoRA down-projection when an adapter runs. */
 #define NLD_TRACE_EMBED 0
 #define NLD_TRACE_QKV 1
 #define NLD_TRACE_ATTENTION 2

@@ -39,31 +39,26 @@ nld_status fail(nld_status st, const char* fmt, ...) {
     } while (0)
 
 // ---------------------------------------------------------------- tracing aid
+// While tracing is on, every launch inside a TraceScope gets its own pair of events,
+// recorded by the launch on its own dispatch (kernel start and end), filed under the
+// scope's kernel class.
 struct TraceRec {
     int cls;
+    bool first;   // first launch of its scope: the scope counts once in its class
     hipEvent_t start, stop;
 };
 bool g_trace_on = false;
 std::vector<TraceRec> g_trace;
+thread_local int g_trace_cls = -1;
+thread_local bool g_trace_scope_new = false;
 
 struct TraceScope {
-    TraceRec rec{};
-    hipStream_t s;
-    bool on;
-    TraceScope(int cls, hipStream_t st) : s(st), on(g_trace_on) {
-        if (!on) return;
-        rec.cls = cls;
-        if (hipEventCreate(&rec.start) != hipSuccess || hipEventCreate(&rec.stop) != hipSuccess) {
-            on = false;
-            return;
-        }
-        (void)hipEventRecord(rec.start, s);
+    int saved;
+    TraceScope(int cls, hipStream_t) : saved(g_trace_cls) {
+        g_trace_cls = cls;
+        g_trace_scope_new = true;
     }
-    ~TraceScope() {
-        if (!on) return;
-        (void)hipEventRecord(rec.stop, s);
-        g_trace.push_back(rec);
-    }
+    ~TraceScope() { g_trace_cls = saved; }
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -73,6 +68,27 @@ int env_int(const char* name, int dflt) {
     const char* v = getenv(name);
     return (v && *v) ? atoi(v) : dflt;
 }
+
+}  // namespace
+
+bool nld::trace_launch_events(hipEvent_t* start, hipEvent_t* stop) {
+    if (!g_trace_on || g_trace_cls < 0) return false;
+    TraceRec r{};
+    r.cls = g_trace_cls;
+    r.first = g_trace_scope_new;
+    g_trace_scope_new = false;
+    if (hipEventCreate(&r.start) != hipSuccess) return false;
+    if (hipEventCreate(&r.stop) != hipSuccess) {
+        (void)hipEventDestroy(r.start);
+        return false;
+    }
+    g_trace.push_back(r);
+    *start = r.start;
+    *stop = r.stop;
+    return true;
+}
+
+namespace {
 
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
@@ -843,7 +859,7 @@ nld_status nld_trace_read(float* ms, int32_t* counts, int32_t n) {
             if (e != hipSuccess) st = fail(NLD_ERR_HIP, "trace event: %s", hipGetErrorString(e));
         }
         ms[r.cls] += t;
-        counts[r.cls] += 1;
+        counts[r.cls] += r.first ? 1 : 0;
         (void)hipEventDestroy(r.start);
         (void)hipEventDestroy(r.stop);
     }

@@ -20,9 +20,21 @@
 
 #include "nld_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 
 namespace nld {
+
+// Every kernel launch goes through here: a plain launch, or, while launch tracing is on,
+// a launch whose start and stop events are recorded on the dispatch itself.
+template <typename... KArgs, typename... Args>
+static void launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, Args... args) {
+    hipEvent_t e0, e1;
+    if (trace_launch_events(&e0, &e1)) hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e0, e1, 0, args...);
+    else kernel<<<grid, block, 0, s>>>(args...);
+}
+
 
 static constexpr uint32_t DEV_BAD_TOKEN = 0x1u;
 static constexpr uint32_t DEV_CAPACITY = 0x2u;
@@ -309,9 +321,9 @@ template <int KS>
 static hipError_t launch_norm_ks(int epi, int waves, int grid, const GemmArgs& a, hipStream_t s) {
     const dim3 blk(waves * 64);
     switch (epi) {
-        case EPI_QKV: gemm_norm_kernel<KS, EPI_QKV><<<grid, blk, 0, s>>>(a); break;
-        case EPI_SWIGLU: gemm_norm_kernel<KS, EPI_SWIGLU><<<grid, blk, 0, s>>>(a); break;
-        case EPI_LMHEAD: gemm_norm_kernel<KS, EPI_LMHEAD><<<grid, blk, 0, s>>>(a); break;
+        case EPI_QKV: launch(gemm_norm_kernel<KS, EPI_QKV>, dim3(grid), dim3(blk), s, a); break;
+        case EPI_SWIGLU: launch(gemm_norm_kernel<KS, EPI_SWIGLU>, dim3(grid), dim3(blk), s, a); break;
+        case EPI_LMHEAD: launch(gemm_norm_kernel<KS, EPI_LMHEAD>, dim3(grid), dim3(blk), s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -542,10 +554,10 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
 
 template <int EPI, int MT, bool XK>
 static hipError_t launch_stream_ct(int ct, int nw, dim3 grid, const GemmArgs& a, hipStream_t s) {
-    if (ct == 1 && nw == 8) gemm_stream_kernel<MT, 1, 8, EPI, XK><<<grid, 512, 0, s>>>(a);
-    else if (ct == 2 && nw == 8) gemm_stream_kernel<MT, 2, 8, EPI, XK><<<grid, 512, 0, s>>>(a);
-    else if (ct == 4 && nw == 4) gemm_stream_kernel<MT, 4, 4, EPI, XK><<<grid, 256, 0, s>>>(a);
-    else if (ct == 1 && nw == 4) gemm_stream_kernel<MT, 1, 4, EPI, XK><<<grid, 256, 0, s>>>(a);
+    if (ct == 1 && nw == 8) launch(gemm_stream_kernel<MT, 1, 8, EPI, XK>, dim3(grid), dim3(512), s, a);
+    else if (ct == 2 && nw == 8) launch(gemm_stream_kernel<MT, 2, 8, EPI, XK>, dim3(grid), dim3(512), s, a);
+    else if (ct == 4 && nw == 4) launch(gemm_stream_kernel<MT, 4, 4, EPI, XK>, dim3(grid), dim3(256), s, a);
+    else if (ct == 1 && nw == 4) launch(gemm_stream_kernel<MT, 1, 4, EPI, XK>, dim3(grid), dim3(256), s, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -949,18 +961,18 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
 
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
     const dim3 grid(a.n_splits + 1, units, zslices);   // prefix splits + the block part
-    if (head_dim == 128 && kh == 2) attention_kernel<128, 2><<<grid, 512, 0, s>>>(a);
-    else if (head_dim == 128 && kh == 1) attention_kernel<128, 1><<<grid, 512, 0, s>>>(a);
-    else if (head_dim == 64 && kh == 2) attention_kernel<64, 2><<<grid, 512, 0, s>>>(a);
-    else if (head_dim == 64 && kh == 1) attention_kernel<64, 1><<<grid, 512, 0, s>>>(a);
+    if (head_dim == 128 && kh == 2) launch(attention_kernel<128, 2>, dim3(grid), dim3(512), s, a);
+    else if (head_dim == 128 && kh == 1) launch(attention_kernel<128, 1>, dim3(grid), dim3(512), s, a);
+    else if (head_dim == 64 && kh == 2) launch(attention_kernel<64, 2>, dim3(grid), dim3(512), s, a);
+    else if (head_dim == 64 && kh == 1) launch(attention_kernel<64, 1>, dim3(grid), dim3(512), s, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s) {
     const dim3 grid(units, rows);
-    if (head_dim == 128) attention_combine_kernel<128><<<grid, 128, 0, s>>>(a);
-    else if (head_dim == 64) attention_combine_kernel<64><<<grid, 64, 0, s>>>(a);
+    if (head_dim == 128) launch(attention_combine_kernel<128>, dim3(grid), dim3(128), s, a);
+    else if (head_dim == 64) launch(attention_combine_kernel<64>, dim3(grid), dim3(64), s, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -1026,7 +1038,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-    embed_kernel<<<a.M, 256, 0, s>>>(a);
+    launch(embed_kernel, dim3(a.M), dim3(256), s, a);
     return hipGetLastError();
 }
 
@@ -1134,7 +1146,7 @@ __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
 
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s) {
     const int threads = a.finish == FINISH_REFRESH ? 64 : 64 * (a.k_blk < 16 ? a.k_blk : 16);
-    finish_kernel<<<a.batch, threads, 0, s>>>(a);
+    launch(finish_kernel, dim3(a.batch), dim3(threads), s, a);
     return hipGetLastError();
 }
 
@@ -1176,7 +1188,7 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
     const size_t total = (size_t)a.n_tiles * a.ksteps * 64;
     size_t blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    pack_kernel<<<(unsigned)blocks, 256, 0, s>>>(a);
+    launch(pack_kernel, dim3((unsigned)blocks), dim3(256), s, a);
     return hipGetLastError();
 }
 
@@ -1189,7 +1201,7 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
     size_t blocks = (n + 255) / 256;
     if (blocks > 4096) blocks = 4096;
     if (blocks == 0) return hipSuccess;
-    fill_zero_kernel<<<(unsigned)blocks, 256, 0, s>>>((uint32_t*)p, n);
+    launch(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), s, (uint32_t*)p, n);
     return hipGetLastError();
 }
 

@@ -217,6 +217,11 @@ struct PackArgs {
     uint4* dst;
 };
 
+// ---------------------------------------------------------------- launch tracing (api.hip)
+// While tracing is on, returns true with a fresh pair of events for the next launch, which
+// then records them on its own dispatch (start and end of the kernel itself).
+bool trace_launch_events(hipEvent_t* start, hipEvent_t* stop);
+
 // ---------------------------------------------------------------- launchers (kernels.hip)
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
