@@ -231,6 +231,8 @@ def main():
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the Mode 2 and LoRA timings (counter runs use this: eager launches only)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run plain copies of this many MiB (reference dispatches for counter runs)")
     args = ap.parse_args()
@@ -317,10 +319,12 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
-        block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
-        m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
-        lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
-        status |= R.read_device_status(ws) | lora_ms["status"]
+        m2_ms = lora_ms = None
+        if not args.no_extras:
+            block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
+            m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
+            lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
+            status |= R.read_device_status(ws) | lora_ms["status"]
 
     ms_per_step = elapsed_ms / steps
     value = 2.0 * B * k / (ms_per_step * 1e-3)
@@ -365,7 +369,9 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "bytes_per_launch": int(kb[dom]), "avg_launch_us": kernels[dom]["avg_us"]},
         "kernels": kernels,
-        "mode2": {
+    }
+    if m2_ms is not None:
+        res["mode2"] = {
             "denoise_step_ms": round(m2_ms["denoise_step"], 4),
             "denoise_hbm_frac": round(pass_bytes(shape, B, k, plens) / (m2_ms["denoise_step"] * 1e-3) / 1e9
                                       / HBM_PEAK_GBS, 4),
@@ -374,16 +380,15 @@ def main():
                                       / HBM_PEAK_GBS, 4),
             "threshold": 0.9,
             "first_step_commits": m2_committed,
-        },
-        "lora_draft": {
+        }
+        res["lora_draft"] = {
             "rank": LORA_RANK, "alpha": LORA_ALPHA,
             "draft_pass_ms": round(lora_ms["draft"], 4),
             "lora_draft_pass_ms": round(lora_ms["lora_draft"], 4),
             "lora_draft_hbm_frac": round((pass_bytes(shape, B, k, plens) + shape.n_layers * 2 * LORA_RANK
                                           * (shape.q_dim + shape.hidden)) / (lora_ms["lora_draft"] * 1e-3) / 1e9
                                          / HBM_PEAK_GBS, 4),
-        },
-    }
+        }
     if not args.no_cpu_baseline:
         del model, cache, ws
         torch.cuda.empty_cache()
