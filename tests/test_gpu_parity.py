@@ -282,6 +282,20 @@ def test_tiny_decode_steps_ar_mode(R, tiny):
     assert R.read_device_status(ws) == 0
 
 
+def test_draft_with_bidir_from_k_is_the_verify_pass(R, tiny):
+    """A draft pass whose bidirectional rows start at k has the causal mask: its logits equal the verify
+    pass's bit for bit (the draft still writes no cache row)."""
+    t = tiny
+    bt = torch.from_numpy(t["block"]).cuda()
+    ws = R.Workspace(t["model"], 1, 8, 256)
+    cache = _tiny_cache_copy(R, t)
+    before = cache.read_kv(0, 128, 136)
+    d = R.block_forward(t["model"], cache, ws, bt, R.DRAFT, 8)[0]
+    assert all(np.array_equal(x, y) for x, y in zip(before, cache.read_kv(0, 128, 136)))
+    v = R.block_forward(t["model"], cache, ws, bt, R.VERIFY)[0]
+    assert torch.equal(d, v)
+
+
 def test_capacity_error_is_reported_not_written(R, tiny):
     """A block that would run past max_len sets the capacity bit; no row beyond the cache is written."""
     t = tiny
@@ -319,7 +333,7 @@ def layer8b(R):
     return dict(shape=shape, w=w, okv=okv, model=model, cache=cache, seed=seed)
 
 
-@pytest.mark.parametrize("k", [8, 16, 32])
+@pytest.mark.parametrize("k", [8, 16, 32, 64])
 @pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
 def test_8b_layer_block_pass(R, layer8b, k, mode):
     t = layer8b
