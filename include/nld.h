@@ -91,7 +91,7 @@ typedef struct {
      * NLD_MODE_DRAFT); verify passes never read it.  A draft pass adds
      * lora_scale * B (A o) to the O projection's output, A = lora_a [lora_rank][n_q_heads*head_dim],
      * B = lora_b [hidden][lora_rank] (standard LoRA, lora_scale = alpha / rank; the paper
-     * uses rank 128, alpha 512).  lora_rank 0 (no adapter) or a multiple of 32. */
+     * uses rank 128, alpha 512).  lora_rank 0 (no adapter) or a multiple of 32 up to 512. */
     int32_t lora_rank;
     float lora_scale;
 } nld_config;

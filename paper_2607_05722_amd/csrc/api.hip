@@ -165,6 +165,7 @@ nld_status check_config(const nld_config* c) {
     if (c->lora_rank < 0 || !(fabsf(c->lora_scale) < INFINITY))
         return fail(NLD_ERR_INVALID_ARG, "lora_rank must be >= 0 and lora_scale finite");
     if (c->lora_rank % 32) return fail(NLD_ERR_SHAPE, "lora_rank (%d) must be a multiple of 32", c->lora_rank);
+    if (c->lora_rank > 512) return fail(NLD_ERR_SHAPE, "lora_rank (%d) must be at most 512", c->lora_rank);
     return NLD_OK;
 }
 

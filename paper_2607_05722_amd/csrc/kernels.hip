@@ -377,11 +377,9 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     const int t0 = blockIdx.x * CT;
     const int m0 = blockIdx.y * 16 * MT;
 
-    // k-steps [0, ksteps) come from (W, A); with XK, [ksteps, ksteps + ksteps2) from (W2, A2)
-    const int KT = XK ? a.ksteps + a.ksteps2 : a.ksteps;
-    const int per = (KT + NW - 1) / NW;
-    const int s_begin = min(KT, wave * per);
-    const int s_end = min(KT, s_begin + per);
+    const int per = (a.ksteps + NW - 1) / NW;
+    const int s_begin = min(a.ksteps, wave * per);
+    const int s_end = min(a.ksteps, s_begin + per);
 
     const uint4* wp[CT];
 #pragma unroll
@@ -396,17 +394,29 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         aok[mt] = m0 + mt * 16 + r < a.M;
         ap[mt] = a.A + (size_t)(blockIdx.y * MT + mt) * a.ksteps * BSTRIDE + (size_t)lane * 8;
     }
-    const uint4* wp2[CT];
-    const uint16_t* ap2[MT];
+    // XK: the second source's k-steps (W2 against A2) go one to a wavefront (wavefront w takes step
+    // w, then w + NW, ...).  They are loaded before the main stream and multiplied after it, so the
+    // main loop is the same as without them.
+    constexpr int XS = XK ? 2 : 1;   // second-source k-steps held per wavefront (at most 2 * NW in all)
+    uint4 xw[XS][CT], xa[XS][MT], xal[XS][MT];
     if constexpr (XK) {
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            const int t = min(t0 + ct, a.n_tiles - 1);
-            wp2[ct] = a.W2 + (size_t)t * a.ksteps2 * 64 + lane;
-        }
+        for (int i = 0; i < XS; ++i) {
+            const int s2 = wave + i * NW;
+            const bool in = s2 < a.ksteps2;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            ap2[mt] = a.A2 + (size_t)(blockIdx.y * MT + mt) * a.ksteps2 * BSTRIDE + (size_t)lane * 8;
+            for (int ct = 0; ct < CT; ++ct) {
+                const int t = min(t0 + ct, a.n_tiles - 1);
+                xw[i][ct] = in ? a.W2[((size_t)t * a.ksteps2 + s2) * 64 + lane] : uint4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint16_t* ap2 = a.A2 + ((size_t)(blockIdx.y * MT + mt) * a.ksteps2 + s2) * BSTRIDE + (size_t)lane * 8;
+                const bool ok = in && aok[mt];
+                xa[i][mt] = ok ? *(const uint4*)ap2 : uint4{0u, 0u, 0u, 0u};
+                xal[i][mt] = ok ? *(const uint4*)(ap2 + SPLIT_LO) : uint4{0u, 0u, 0u, 0u};
+            }
+        }
     }
 
     f32x4_t acc[MT][CT], accl[SPLIT ? MT : 1][SPLIT ? CT : 1];
@@ -446,21 +456,14 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         for (int u = 0; u < U; ++u) {
             const int ss = s + u;
             const bool in = ss < s_end;
-            // second source: wave-uniform; its columns are whole k-steps, never past its end
-            const bool second = XK && ss >= a.ksteps;
-            const int s2 = ss - a.ksteps;
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                const uint4* src = second ? wp2[ct] + (size_t)s2 * 64 : wp[ct] + (size_t)ss * 64;
-                buf.w[u][ct] = in ? *src : zero4;
-            }
+            for (int ct = 0; ct < CT; ++ct) buf.w[u][ct] = in ? wp[ct][(size_t)ss * 64] : zero4;
             const int kcol = ss * 32 + 8 * g;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const bool ok = in && aok[mt] && (second || kcol < a.K);
-                const uint16_t* asrc = second ? ap2[mt] + (size_t)s2 * BSTRIDE : ap[mt] + (size_t)ss * BSTRIDE;
-                buf.x[u][mt] = ok ? *(const uint4*)asrc : zero4;
-                if constexpr (SPLIT) buf.xl[u][mt] = ok ? *(const uint4*)(asrc + SPLIT_LO) : zero4;
+                const bool ok = in && aok[mt] && kcol < a.K;
+                buf.x[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE) : zero4;
+                if constexpr (SPLIT) buf.xl[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * BSTRIDE + SPLIT_LO) : zero4;
             }
         }
     };
@@ -486,6 +489,17 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         compute(b1);
     }
 
+    if constexpr (XK) {
+#pragma unroll
+        for (int i = 0; i < XS; ++i)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+                    acc[mt][ct] = mfma_16x16x32(xa[i][mt], xw[i][ct], acc[mt][ct]);
+                    accl[mt][ct] = mfma_16x16x32(xal[i][mt], xw[i][ct], accl[mt][ct]);
+                }
+    }
     if constexpr (SPLIT) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)

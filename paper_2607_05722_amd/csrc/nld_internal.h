@@ -95,9 +95,10 @@ struct GemmArgs {
     int n_tiles;
     int ksteps;          // ceil(K / 32)
     unsigned* tile_ctr;  // normed GEMM: dynamic tile counter (zeroed by the embedding kernel each pass)
-    // Second reduction source (streamed GEMM only): k-steps [ksteps, ksteps + ksteps2)
-    // read W2 (packed, ksteps2 steps per tile) against A2 (split, ksteps2 steps per row
-    // tile).  The draft pass's O projection uses it for the LoRA up-projection.
+    // Second reduction source (streamed GEMM only, ksteps2 <= 2 * wavefronts): the sum
+    // continues over ksteps2 more k-steps of W2 (packed, ksteps2 steps per tile) against A2
+    // (split, ksteps2 steps per row tile).  The draft pass's O projection uses it for the
+    // LoRA up-projection.
     const uint4* W2;
     const uint16_t* A2;
     int ksteps2;

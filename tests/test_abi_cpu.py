@@ -144,6 +144,7 @@ def test_draft_and_verify_validation():
 def test_lora_config_validation():
     lib = C.load()
     assert fake_model(lora_rank=48, lora_scale=4.0)[0] == C.NLD_ERR_SHAPE
+    assert fake_model(lora_rank=544, lora_scale=4.0)[0] == C.NLD_ERR_SHAPE
     assert fake_model(lora_rank=-32, lora_scale=4.0)[0] == C.NLD_ERR_INVALID_ARG
     assert fake_model(lora_rank=32, lora_scale=float("inf"))[0] == C.NLD_ERR_INVALID_ARG
     # a rank without adapter weights (fake_model leaves lora_a / lora_b NULL)
