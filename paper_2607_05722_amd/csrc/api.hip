@@ -61,6 +61,8 @@ struct TraceScope {
     ~TraceScope() { g_trace_cls = saved; }
 };
 
+int device_cus();
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
@@ -109,7 +111,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.lm_tiles = cdiv(c.vocab, 16);
     L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
     // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
-    const int target = env_int("NLD_ATTN_TARGET_WG", 256);
+    const int target = env_int("NLD_ATTN_TARGET_WG", device_cus());
     int ns = target / (L.units * L.attn_z) - 1;    // one workgroup per (unit, row slice) is the block part
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
@@ -187,11 +189,26 @@ bool plan_norm(int epi, int M, int ksteps, int* ks, int* waves) {
     return false;
 }
 
+// Compute units of the current device (queried once per device; NLD_CUS overrides).
+int device_cus() {
+    const int forced = env_int("NLD_CUS", 0);
+    if (forced > 0) return forced;
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        cached[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+                          ? n : 256;
+    }
+    return cached[dev];
+}
+
 // Workgroups of the normed GEMM: one per CU, but at least two tiles per workgroup on
 // average (each workgroup loads the whole operand once); tiles beyond the first one per
 // workgroup are handed out dynamically.
 int norm_grid(int n_tiles) {
-    const int cus = env_int("NLD_CUS", 256);
+    const int cus = device_cus();
     const int half = (n_tiles + 1) / 2;
     return half < cus ? half : cus;
 }
