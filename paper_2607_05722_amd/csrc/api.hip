@@ -101,7 +101,8 @@ struct Layout {
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     Layout L{};
     L.M = batch * k;
-    L.Mpad = cdiv(L.M, 64) * 64;
+    // operand rows: whole 64-row groups, or whole 128-row tiles of the tiled GEMM (M > 64)
+    L.Mpad = L.M > 64 ? cdiv(L.M, gemm_tile_row_pad()) * gemm_tile_row_pad() : cdiv(L.M, 64) * 64;
     L.units = batch * c.n_kv_heads;
     const int G = c.n_q_heads / c.n_kv_heads;
     L.row_tiles = cdiv(G * k, 16);
@@ -110,8 +111,12 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.rows_pad = L.attn_z * (8 / L.attn_kh) * 16;
     L.lm_tiles = cdiv(c.vocab, 16);
     L.lm_parts = L.lm_tiles;  // upper bound on argmax partials per row (one per LM-head workgroup)
-    // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys
-    const int target = env_int("NLD_ATTN_TARGET_WG", device_cus());
+    // key splits: aim for about `target` workgroups, chunks a multiple of 64 keys.  One
+    // workgroup per CU while there are few (unit, row slice) pairs (batch 1: each workgroup
+    // is then a short latency chain); up to four per CU when there are many, so that long
+    // and ragged key ranges are cut finer than one per CU.
+    const int pairs = L.units * L.attn_z;
+    const int target = env_int("NLD_ATTN_TARGET_WG", device_cus() * std::min(4, std::max(1, pairs / 16)));
     int ns = target / (L.units * L.attn_z) - 1;    // one workgroup per (unit, row slice) is the block part
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
@@ -278,6 +283,18 @@ nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, 
     return NLD_OK;
 }
 
+// The tiled GEMM takes every projection with more than 64 rows whose shape it supports.
+bool use_tile(const GemmArgs& g) {
+    return !env_int("NLD_NO_TILE_GEMM", 0) && !g.W2 && gemm_tile_supported(g.M, g.K, g.ksteps);
+}
+
+// Residual projections (O, down): the tiled GEMM when it applies, else the streamed one.
+hipError_t resid_gemm(const GemmArgs& g, hipStream_t s) {
+    if (use_tile(g)) return launch_gemm_tile(EPI_RESID, g, s);
+    const StreamPlan p = plan_stream(EPI_RESID, g.M, g.n_tiles);
+    return launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, g, s);
+}
+
 // One projection whose operand is RMSNorm(x) (QKV, gate/up, LM head): the normed
 // multi-tile kernel for M <= 16, else the streamed kernel (both read the bf16
 // operand and the row statistics the producer of x wrote).
@@ -291,6 +308,11 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
         if (parts_out) *parts_out = grid;
         g.n_parts = grid;
         return launch_gemm_norm(epi, ks, waves, grid, g, s);
+    }
+    if (use_tile(g)) {
+        g.n_parts = gemm_tile_parts(g.n_tiles);
+        if (parts_out) *parts_out = g.n_parts;
+        return launch_gemm_tile(epi, g, s);
     }
     const StreamPlan p = plan_stream(epi, g.M, g.n_tiles);
     if (parts_out) *parts_out = p.gx;
@@ -432,8 +454,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         go.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_O_PROJ, s);
-            const StreamPlan p = plan_stream(EPI_RESID, M, go.n_tiles);
-            HIP_TRY(launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, go, s));
+            HIP_TRY(resid_gemm(go, s));
         }
 
         GemmArgs gu{};
@@ -464,8 +485,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gd.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_DOWN, s);
-            const StreamPlan p = plan_stream(EPI_RESID, M, gd.n_tiles);
-            HIP_TRY(launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, gd, s));
+            HIP_TRY(resid_gemm(gd, s));
         }
     }
 

@@ -603,6 +603,213 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
 }
 
 // =====================================================================================
+// Tiled GEMM for many rows (M > 64), where the projections approach the MFMA ridge: a
+// workgroup computes a 128-row x 128-column output tile over the whole reduction, so the
+// weights stream once per 128 rows and the operand once per 128 columns.  Per stage of
+// two k-steps the operand's eight row tiles (split: hi and lo) and the weights' eight
+// column tiles are copied into LDS, double buffered, with the next stage's global loads
+// in flight in registers while the current one is multiplied.  Wavefront w multiplies
+// row tiles 2(w/2), +1 against column tiles 4(w%2) .. +3 (8 MFMAs per operand half and
+// k-step).  Workgroups are ordered so that the row groups sharing a column group run
+// next to each other on one XCD (workgroup b runs on XCD b % 8) and find its weight
+// tiles in that XCD's L2.  Epilogues as in the other GEMMs.
+// =====================================================================================
+namespace tile {
+constexpr int BR = 8;                        // row tiles per workgroup
+constexpr int BC = 8;                        // column tiles per workgroup
+constexpr int KS = 2;                        // k-steps per stage
+constexpr int A_CHUNKS = BR * KS * 2;        // 1 KiB operand blocks per stage (hi and lo)
+constexpr int W_CHUNKS = BC * KS;            // 1 KiB weight blocks per stage
+constexpr int CHUNKS = A_CHUNKS + W_CHUNKS;
+constexpr int NT = 512;
+constexpr int CPT = CHUNKS * 64 / NT;        // 16-byte pieces per thread per stage
+static_assert(A_CHUNKS * 64 % NT == 0 && CHUNKS * 64 % NT == 0, "pieces per thread must split by kind");
+}  // namespace tile
+
+template <int EPI>
+__global__ void __launch_bounds__(512) gemm_tile_kernel(GemmArgs a, int R, int C) {
+    using namespace tile;
+    constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LMHEAD;
+    __shared__ uint4 lds[2][CHUNKS * 64];
+    __shared__ float inv_s[BR * 16];
+    __shared__ int pos_s[BR * 16];
+    __shared__ unsigned long long key_s[BR * 16];
+    __shared__ float2 lse_s[BR * 16][BC];
+
+    const int b = blockIdx.x, xcd = b & 7, gi = b >> 3;
+    const int rg = gi % R, c = (gi / R) * 8 + xcd;
+    if (c >= C) return;   // the whole workgroup leaves: the grid covers whole groups of 8 column groups
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int m0 = rg * BR * 16;
+
+    if constexpr (EPI == EPI_LMHEAD) {
+        if (threadIdx.x < BR * 16) {
+            key_s[threadIdx.x] = 0ull;
+#pragma unroll
+            for (int j = 0; j < BC; ++j) lse_s[threadIdx.x][j] = float2{-INFINITY, 0.f};
+        }
+    }
+    if constexpr (NORMED) rms_scales(a, m0, BR * 16, inv_s);
+    if constexpr (EPI == EPI_QKV) {
+        if (threadIdx.x < BR * 16) {
+            const int m = min(m0 + (int)threadIdx.x, a.M - 1);
+            pos_s[threadIdx.x] = committed_length(a.lengths, m / a.k_blk, a.max_len, a.status) + m % a.k_blk;
+        }
+    }
+
+    // Stage pieces: thread (wave, lane) copies piece q = 1 KiB block wave + 8q, 16 bytes at
+    // lane.  Blocks 0 .. A_CHUNKS-1 are operand blocks (row tile, k-step, half), the rest
+    // weight blocks (column tile, k-step).  The launcher guarantees whole stages (ksteps a
+    // multiple of KS, K a multiple of 32) and operand rows allocated up to a multiple of
+    // 128; column tiles past the end are read clamped and their outputs dropped.  So every
+    // load is unconditional and in bounds.
+    static_assert(A_CHUNKS % 8 == 0 && CHUNKS == 8 * CPT, "8 blocks per piece index");
+    const int nst = a.ksteps / KS;
+    const uint4* srcp[CPT];   // stage 0 address of each piece
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+        const int chunk = wave + 8 * q;
+        if (q < A_CHUNKS / 8) {
+            const int rt = chunk / (KS * 2), ks = (chunk / 2) % KS, half = chunk & 1;
+            srcp[q] = (const uint4*)(a.A + ((size_t)((m0 / 16 + rt) * a.ksteps + ks) * 2 + half) * 512) + lane;
+        } else {
+            const int wck = chunk - A_CHUNKS, ct = wck / KS, ks = wck % KS;
+            srcp[q] = a.W + ((size_t)min(c * BC + ct, a.n_tiles - 1) * a.ksteps + ks) * 64 + lane;
+        }
+    }
+    // stage st: operand blocks advance by KS k-steps of 2 KiB, weight blocks by KS of 1 KiB
+    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+#define NLD_TILE_GLOAD(st, dst)                                                            \
+    _Pragma("unroll") for (int q = 0; q < CPT; ++q)                                         \
+        dst[q] = *(const u32x4_t*)(srcp[q] + (size_t)(st) * KS * (q < A_CHUNKS / 8 ? 128 : 64))
+#define NLD_TILE_LSTORE(v, buf) \
+    _Pragma("unroll") for (int q = 0; q < CPT; ++q) *(u32x4_t*)&lds[buf][threadIdx.x + q * NT] = v[q]
+
+    // one accumulator per output tile takes both operand halves (eight independent tiles keep
+    // the MFMA pipeline busy between the two dependent products)
+    f32x4_t acc[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            uint4 ah[2], al[2], w[4];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int rt = 2 * wr + i;
+                ah[i] = lds[buf][((rt * KS + ks) * 2 + 0) * 64 + lane];
+                al[i] = lds[buf][((rt * KS + ks) * 2 + 1) * 64 + lane];
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) w[j] = lds[buf][(A_CHUNKS + (4 * wc + j) * KS + ks) * 64 + lane];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(ah[i], w[j], acc[i][j]);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(al[i], w[j], acc[i][j]);
+        }
+    };
+
+    // Stage s is multiplied from LDS buffer s & 1 while stage s+1 waits in registers and
+    // stage s+2 is in flight (unrolled by two so that no register copy waits on a load still
+    // in flight; loads past the last stage re-read it and are never stored).
+    u32x4_t r0[CPT], r1[CPT];
+    NLD_TILE_GLOAD(0, r0);
+    NLD_TILE_GLOAD(min(1, nst - 1), r1);
+    NLD_TILE_LSTORE(r0, 0);
+    __syncthreads();
+    for (int st = 0; st < nst; st += 2) {
+        NLD_TILE_GLOAD(min(st + 2, nst - 1), r0);
+        compute(0);
+        if (st + 1 < nst) { NLD_TILE_LSTORE(r1, 1); }
+        __syncthreads();
+        if (st + 1 >= nst) break;
+        NLD_TILE_GLOAD(min(st + 3, nst - 1), r1);
+        compute(1);
+        if (st + 2 < nst) { NLD_TILE_LSTORE(r0, 0); }
+        __syncthreads();
+    }
+#undef NLD_TILE_GLOAD
+#undef NLD_TILE_LSTORE
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const f32x4_t v = acc[i][j];
+            const int rt = 2 * wr + i, ct = 4 * wc + j;
+            const int t = c * BC + ct;
+            if (t >= a.n_tiles) continue;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int ml = rt * 16 + 4 * g + e;
+                const int m = m0 + ml;
+                if constexpr (EPI == EPI_RESID) {
+                    const int N = a.n_tiles * 16;
+                    const float xr = m < a.M ? a.x[(size_t)m * N + t * 16 + r] : 0.f;
+                    epi_resid(a, v[e], m, t, lane, xr, bf16_to_f32(a.gain_next[t * 16 + r]));
+                } else if constexpr (EPI == EPI_QKV) {
+                    epi_qkv(a, v[e] * inv_s[ml], m, t, lane, pos_s[ml]);
+                } else if constexpr (EPI == EPI_SWIGLU) {
+                    epi_swiglu(a, v[e] * inv_s[ml], m, t, lane);
+                } else {
+                    float2 tl;
+                    const unsigned long long key = epi_lmhead(a, v[e] * inv_s[ml], m, t, lane, &tl);
+                    if (r == 0) {
+                        atomicMax(&key_s[ml], key);
+                        if (a.part_lse) lse_s[ml][ct] = tl;   // each (row, column tile) is finished once
+                    }
+                }
+            }
+        }
+    if constexpr (EPI == EPI_LMHEAD) {
+        __syncthreads();
+        if (threadIdx.x < BR * 16) {
+            const int m = m0 + threadIdx.x;
+            if (m < a.M) {
+                a.part_keys[(size_t)m * a.n_parts + c] = key_s[threadIdx.x];
+                if (a.part_lse) {
+                    float2 st = float2{-INFINITY, 0.f};
+#pragma unroll
+                    for (int j = 0; j < BC; ++j) st = lse_merge(st, lse_s[threadIdx.x][j]);
+                    a.part_lse[(size_t)m * a.n_parts + c] = st;
+                }
+            }
+        }
+    }
+}
+
+int gemm_tile_parts(int n_tiles) { return (n_tiles + tile::BC - 1) / tile::BC; }
+
+bool gemm_tile_supported(int M, int K, int ksteps) {
+    return M > 64 && K % 32 == 0 && ksteps % tile::KS == 0 && ksteps >= tile::KS;
+}
+
+int gemm_tile_row_pad() { return tile::BR * 16; }
+
+hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s) {
+    if (!gemm_tile_supported(a.M, a.K, a.ksteps) || a.W2) return hipErrorInvalidValue;
+    const int R = (a.M + tile::BR * 16 - 1) / (tile::BR * 16);
+    const int C = gemm_tile_parts(a.n_tiles);
+    const dim3 grid((unsigned)(R * ((C + 7) / 8) * 8)), blk(tile::NT);
+    switch (epi) {
+        case EPI_QKV: launch(gemm_tile_kernel<EPI_QKV>, grid, blk, s, a, R, C); break;
+        case EPI_RESID: launch(gemm_tile_kernel<EPI_RESID>, grid, blk, s, a, R, C); break;
+        case EPI_SWIGLU: launch(gemm_tile_kernel<EPI_SWIGLU>, grid, blk, s, a, R, C); break;
+        case EPI_LMHEAD: launch(gemm_tile_kernel<EPI_LMHEAD>, grid, blk, s, a, R, C); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// =====================================================================================
 // Block-masked GQA attention.  Workgroup = (key split, sequence x KV head, row slice);
 // one compute wavefront per 16 query rows of the GQA group (rows = heads of the
 // group x block rows).  The committed prefix [0, P) is cut into key splits that

@@ -236,6 +236,14 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // With a.W2 set (EPI_RESID only) the reduction continues over the second source.
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
+// Tiled GEMM for M > 64 (no second source): 128 x 128 output tiles.  Needs K % 32 == 0, an
+// even k-step count and the A operand allocated for rows up to a multiple of
+// gemm_tile_row_pad().  gemm_tile_parts gives the number of column groups (the argmax
+// partials per row of the LM head).
+bool gemm_tile_supported(int M, int K, int ksteps);
+int gemm_tile_row_pad();
+int gemm_tile_parts(int n_tiles);
+hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s);
 // kh: key halves per stage (2 when the unit has at most 4 row tiles, else 1); 8 wavefronts per workgroup.
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);

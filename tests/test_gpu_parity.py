@@ -50,7 +50,7 @@ INT_SHAPE = ModelShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_d
                        rms_eps=0.0)
 
 
-@pytest.mark.parametrize("k", [1, 8, 40])
+@pytest.mark.parametrize("k", [1, 8, 40, 64])
 def test_lm_head_integer_exact(R, k):
     """Embedding gather, LM-head packing/tiling (ragged vocab 1000) and the fused argmax: the logits are
     exact integers on both sides, so they must agree bit for bit, ties included (lowest index wins)."""
@@ -355,4 +355,46 @@ def test_8b_layer_block_pass(R, layer8b, k, mode):
         assert rel_err(O.bf16_bits_to_float(vg), nv[0]) < TOL
     else:                    # a draft pass writes no cache row
         assert np.array_equal(kg, before[0]) and np.array_equal(vg, before[1])
+    assert R.read_device_status(ws) == 0
+
+
+@pytest.fixture(scope="module")
+def layer8b_b4(R):
+    """One 8B-shaped layer, batch 4 with ragged prefixes: 128 block rows at k=32 (the tiled GEMM path)."""
+    wl = WORKLOADS["8b_layer"]
+    shape, seed = wl.shape, wl.seed
+    lengths = np.array([2048, 1000, 64, 1537])
+    src = LazyWeights(shape, seed)
+    kb, vb = prefix_kv(shape, seed, 0, 4, int(lengths.max()))
+    w = O.OracleWeights(shape, src, np.float32)
+    okv = O.OracleKV(shape, 4, 2048 + 64, np.float32)
+    okv.set_prefix_bf16(0, kb, vb, lengths)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, 4, 2048 + 64)
+    cache.load_prefix(0, kb, vb)
+    cache.set_lengths(lengths)
+    return dict(shape=shape, w=w, okv=okv, model=model, cache=cache, seed=seed, lengths=lengths)
+
+
+@pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
+def test_8b_layer_batched_block_pass(R, layer8b_b4, mode):
+    """128 rows (batch 4, k=32, ragged prefixes 64..2048): every projection runs on the tiled MFMA GEMM;
+    logits, argmax and the verify pass's K/V rows against the oracle."""
+    t = layer8b_b4
+    shape, k = t["shape"], 32
+    tok = synth_tokens(shape, t["seed"], "8b_layer.b4.block", (4, k))
+    ref, nk, nv = O.block_forward(t["w"], t["okv"], tok, mode)
+    ws = R.Workspace(t["model"], 4, k, t["cache"].max_len)
+    logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(tok).cuda(),
+                                 R.VERIFY if mode == O.VERIFY else R.DRAFT)
+    g = logits.cpu().numpy()
+    e = rel_err(g, ref)
+    log("8b_layer batch 4 k=32 %s: rel err %.3e" % (mode, e))
+    assert e <= TOL
+    check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+    if mode == O.VERIFY:
+        for b, P in enumerate(t["lengths"]):
+            kg, vg = t["cache"].read_kv(0, int(P), int(P) + k)
+            assert rel_err(O.bf16_bits_to_float(kg[b:b + 1]), nk[0][b:b + 1]) < TOL
+            assert rel_err(O.bf16_bits_to_float(vg[b:b + 1]), nv[0][b:b + 1]) < TOL
     assert R.read_device_status(ws) == 0
