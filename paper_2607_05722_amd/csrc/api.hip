@@ -95,7 +95,9 @@ namespace {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
-    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, lora_t, drafts, total;
+    int n_sk_ctr, sk_ctr0;   // split-K residual GEMM: counters (one per column group) from tile counter sk_ctr0
+    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, sk_part, lora_t, drafts,
+        total;
 };
 
 Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
@@ -144,7 +146,15 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
     L.lse = take(8 * L.Mpad * (size_t)L.lm_parts);   // softmax statistics per argmax partial (denoising)
     L.rope = take(8 * L.Mpad * (size_t)(c.head_dim / 2));
-    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1));   // per pass: QKV and gate/up of every layer, LM head
+    // split-K GEMM (M <= 32; the O, down and QKV projections): one counter per column group
+    // of at least 2 tiles, and the partials of up to SPLITK_MAX slices of 32-row groups
+    const int sk_tiles = std::max((int)H / 16, (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim / 16);
+    L.n_sk_ctr = L.M <= 32 ? cdiv(sk_tiles, 2) : 0;
+    L.sk_ctr0 = 2 * c.n_layers + 1;
+    // per pass: QKV and gate/up of every layer, LM head; then the split-K counters
+    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr));
+    // partials: whole column groups (at most 2 * n_sk_ctr + 4 tiles of 16) x 32 rows x slices
+    L.sk_part = take(L.M <= 32 ? 4 * (size_t)(2 * L.n_sk_ctr + 4) * 16 * 32 * SPLITK_MAX : 0);
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
     L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
@@ -288,9 +298,45 @@ bool use_tile(const GemmArgs& g) {
     return !env_int("NLD_NO_TILE_GEMM", 0) && !g.W2 && gemm_tile_supported(g.M, g.K, g.ksteps);
 }
 
-// Residual projections (O, down): the tiled GEMM when it applies, else the streamed one.
-hipError_t resid_gemm(const GemmArgs& g, hipStream_t s) {
+// Split-K plan of a projection with at most 32 rows: ct column tiles per workgroup and
+// ksplit K slices, so that column groups x slices is about one workgroup per CU, with
+// every wavefront (8 per workgroup) getting at least two k-steps.  Defaults per
+// projection (measured on MI355X at the 8B shapes): O 4 tiles; down 2 tiles; QKV off
+// (the normed multi-tile kernel is faster there).  Environment overrides:
+// NLD_SPLITK_<O|DOWN|QKV> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
+// NLD_SPLITK / NLD_SPLITK_CT for every projection at once, NLD_NO_SPLITK = 1: off.
+enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2 };
+
+bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct, int* ksplit) {
+    if (g.W2 || L.n_sk_ctr == 0 || env_int("NLD_NO_SPLITK", 0)) return false;
+    static const char* names[] = {"NLD_SPLITK_O", "NLD_SPLITK_DOWN", "NLD_SPLITK_QKV"};
+    static const int dflt_ct[] = {4, 2, 0};
+    int c = dflt_ct[kind], ks = 0;
+    const char* v = getenv(names[kind]);
+    if (v && *v) {
+        c = atoi(v);
+        const char* comma = strchr(v, ',');
+        ks = comma ? atoi(comma + 1) : 0;
+    }
+    c = env_int("NLD_SPLITK_CT", c);
+    ks = env_int("NLD_SPLITK", ks);
+    if (c <= 0 || !gemm_splitk_supported(epi, g.M, c)) return false;
+    const int groups = cdiv(g.n_tiles, c);
+    if (groups > L.n_sk_ctr) return false;
+    if (ks <= 0) ks = std::min(std::max(1, (device_cus() + groups / 2) / groups), std::max(1, g.ksteps / 16));
+    *ct = c;
+    *ksplit = std::max(1, std::min(std::min(ks, SPLITK_MAX), g.ksteps));
+    return true;
+}
+
+// Residual projections (O, down): the tiled GEMM when it applies, the split-K GEMM for
+// up to 32 rows, else the streamed one.
+hipError_t resid_gemm(int kind, const GemmArgs& g, void* ws, const Layout& L, hipStream_t s) {
     if (use_tile(g)) return launch_gemm_tile(EPI_RESID, g, s);
+    int ct = 0, ksplit = 0;
+    if (plan_splitk(kind, EPI_RESID, g, L, &ct, &ksplit))
+        return launch_gemm_splitk(EPI_RESID, ct, ksplit, g, at<float>(ws, L.sk_part),
+                                  at<unsigned>(ws, L.tile_ctr) + L.sk_ctr0, s);
     const StreamPlan p = plan_stream(EPI_RESID, g.M, g.n_tiles);
     return launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, g, s);
 }
@@ -302,7 +348,10 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     g.A = at<uint16_t>(ws, L.xg);
     g.part_ss = at<float>(ws, L.part_ss);
     g.n_ss = g.K / 16;
-    int ks = 0, waves = 0;
+    int ks = 0, waves = 0, ct = 0, ksplit = 0;
+    if (epi == EPI_QKV && plan_splitk(SK_QKV, epi, g, L, &ct, &ksplit))
+        return launch_gemm_splitk(epi, ct, ksplit, g, at<float>(ws, L.sk_part),
+                                  at<unsigned>(ws, L.tile_ctr) + L.sk_ctr0, s);
     if (plan_norm(epi, g.M, g.ksteps, &ks, &waves)) {
         const int grid = norm_grid(g.n_tiles);
         if (parts_out) *parts_out = grid;
@@ -347,7 +396,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.status = status;
     e.rope = at<float2>(ws, L.rope);
     e.tile_ctr = at<unsigned>(ws, L.tile_ctr);
-    e.n_tile_ctr = 2 * c.n_layers + 1;
+    e.n_tile_ctr = 2 * c.n_layers + 1 + L.n_sk_ctr;
     e.lengths = kv->lengths;
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;
@@ -454,7 +503,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         go.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_O_PROJ, s);
-            HIP_TRY(resid_gemm(go, s));
+            HIP_TRY(resid_gemm(SK_O, go, ws, L, s));
         }
 
         GemmArgs gu{};
@@ -485,7 +534,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gd.part_ss_out = at<float>(ws, L.part_ss);
         {
             TraceScope ts(NLD_TRACE_DOWN, s);
-            HIP_TRY(resid_gemm(gd, s));
+            HIP_TRY(resid_gemm(SK_DOWN, gd, ws, L, s));
         }
     }
 

@@ -603,6 +603,205 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
 }
 
 // =====================================================================================
+// Split-K GEMM (O and down projections with the residual epilogue, and the normed QKV
+// projection; M <= 32).  Workgroup (column group cg,
+// K slice ks) multiplies its slice of the operand against CT column tiles, so the
+// operand is read once per CT tiles and K slice instead of once per tile (the split
+// operand is twice as large as the weights it multiplies in these projections).  The
+// NW wavefronts cut the slice further and meet in LDS.  With ksplit > 1 the workgroup's
+// partial [16*MT rows][16*CT columns] goes to the workspace with agent-scope stores
+// (written through to memory, so that every XCD sees them); once every lane's stores
+// are acknowledged, one atomic on the group's counter counts the workgroup in.  The
+// workgroup that arrives last reads the other partials with agent-scope loads (which
+// do not hit stale lines of its own L2), adds the ksplit partials in slice order (the
+// sum does not depend on which workgroup is last), sets the counter back to zero for
+// the next launch and runs the residual epilogue.  No workgroup ever waits for
+// another: there is no spin and no cache-wide fence.
+// =====================================================================================
+template <int MT, int CT, int NW, int EPI>
+__global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float* part, unsigned* ctr, int ksplit) {
+    typedef Batch<MT, CT, true> B;
+    constexpr int U = B::U;
+    constexpr int NTL = MT * CT;   // output tiles of the workgroup; wavefront w < NTL finishes tile w
+    constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU;
+    static_assert(NTL <= NW, "one wavefront per output tile in the epilogue");
+    static_assert(EPI == EPI_RESID || NORMED, "residual, QKV or SwiGLU epilogue");
+    __shared__ f32x4_t red[NW][NTL][64];
+    __shared__ float inv_s[16 * MT];
+    __shared__ int last_s;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int cg = blockIdx.x, ks = blockIdx.y;
+    const int t0 = cg * CT;
+    const int N = a.n_tiles * 16;
+
+    // the workgroup's k-steps [kb, ke), then the wavefront's share [s_begin, s_end)
+    const int per_wg = (a.ksteps + ksplit - 1) / ksplit;
+    const int kb = min(a.ksteps, ks * per_wg), ke = min(a.ksteps, kb + per_wg);
+    const int per = (ke - kb + NW - 1) / NW;
+    const int s_begin = min(ke, kb + wave * per);
+    const int s_end = min(ke, s_begin + per);
+
+    // epilogue inputs of this wavefront's tile, fetched up front: residual rows 4g + i
+    // of the tile and the next RMSNorm gain of column r
+    const int my_mt = wave / CT, my_t = t0 + wave % CT;
+    float xres[4] = {0.f, 0.f, 0.f, 0.f}, gn = 0.f;
+    if (EPI == EPI_RESID && wave < NTL && my_t < a.n_tiles) {
+        gn = bf16_to_f32(a.gain_next[my_t * 16 + r]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = 16 * my_mt + 4 * g + i;
+            if (m < a.M) xres[i] = a.x[(size_t)m * N + my_t * 16 + r];
+        }
+    }
+
+    const uint4* wp[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) wp[ct] = a.W + (size_t)min(t0 + ct, a.n_tiles - 1) * a.ksteps * 64 + lane;
+    const uint16_t* ap[MT];
+    bool aok[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        aok[mt] = mt * 16 + r < a.M;
+        ap[mt] = a.A + (size_t)mt * a.ksteps * 1024 + (size_t)lane * 8;
+    }
+
+    f32x4_t acc[MT][CT], accl[MT][CT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = accl[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const uint4 zero4 = {0u, 0u, 0u, 0u};
+    auto load = [&](int s, B& buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ss = s + u;
+            const bool in = ss < s_end;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) buf.w[u][ct] = in ? wp[ct][(size_t)ss * 64] : zero4;
+            const int kcol = ss * 32 + 8 * g;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const bool ok = in && aok[mt] && kcol < a.K;
+                buf.x[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * 1024) : zero4;
+                buf.xl[u][mt] = ok ? *(const uint4*)(ap[mt] + (size_t)ss * 1024 + SPLIT_LO) : zero4;
+            }
+        }
+    };
+    auto compute = [&](const B& buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+                    acc[mt][ct] = mfma_16x16x32(buf.x[u][mt], buf.w[u][ct], acc[mt][ct]);
+                    accl[mt][ct] = mfma_16x16x32(buf.xl[u][mt], buf.w[u][ct], accl[mt][ct]);
+                }
+    };
+
+    B b0, b1;
+    load(s_begin, b0);
+    if constexpr (NORMED) rms_scales(a, 0, 16 * MT, inv_s);   // visible after the barrier below
+    for (int s = s_begin; s < s_end; s += 2 * U) {
+        load(s + U, b1);
+        compute(b0);
+        load(s + 2 * U, b0);
+        compute(b1);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) red[wave][mt * CT + ct][lane] = acc[mt][ct] + accl[mt][ct];
+    __syncthreads();
+
+    // the workgroup's partial of tile `wave` (fixed order over the wavefronts)
+    f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+    if (wave < NTL) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += red[w][wave][lane];
+    }
+    if (ksplit > 1) {
+        typedef unsigned long long u64;
+        u64* pp = (u64*)(part + ((((size_t)cg * ksplit + ks) * NTL + wave) * 64 + lane) * 4);
+        if (wave < NTL) {
+            __hip_atomic_store(pp, __builtin_bit_cast(u64, f32x2_t{v[0], v[1]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(pp + 1, __builtin_bit_cast(u64, f32x2_t{v[2], v[3]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // every lane's stores are acknowledged before the workgroup counts itself in
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            last_s = __hip_atomic_fetch_add(ctr + cg, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(ksplit - 1);
+        __syncthreads();
+        if (!last_s) return;
+        if (threadIdx.x == 0) __hip_atomic_exchange(ctr + cg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (wave < NTL) {
+            f32x4_t sum = {0.f, 0.f, 0.f, 0.f};
+            for (int sl = 0; sl < ksplit; ++sl) {
+                if (sl == ks) {
+                    sum += v;
+                    continue;
+                }
+                const u64* q = (const u64*)(part + ((((size_t)cg * ksplit + sl) * NTL + wave) * 64 + lane) * 4);
+                const f32x2_t lo = __builtin_bit_cast(f32x2_t, __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const f32x2_t hi = __builtin_bit_cast(f32x2_t, __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                sum += f32x4_t{lo[0], lo[1], hi[0], hi[1]};
+            }
+            v = sum;
+        }
+    }
+    if (wave >= NTL || my_t >= a.n_tiles) return;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = 16 * my_mt + 4 * g + i;
+        if constexpr (EPI == EPI_RESID) {
+            epi_resid(a, v[i], m, my_t, lane, xres[i], gn);
+        } else if constexpr (EPI == EPI_QKV) {
+            const int mc = min(m, a.M - 1);
+            const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
+            epi_qkv(a, v[i] * inv_s[m], m, my_t, lane, pos);
+        } else {
+            epi_swiglu(a, v[i] * inv_s[m], m, my_t, lane);
+        }
+    }
+}
+
+bool gemm_splitk_supported(int epi, int M, int ct) {
+    return (epi == EPI_RESID || epi == EPI_QKV || epi == EPI_SWIGLU) && M >= 1 && M <= 32 && ct >= 2 && ct <= 4;
+}
+
+template <int EPI, int CT>
+static void launch_splitk_ct(dim3 grid, bool two, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
+                             hipStream_t s) {
+    if (two) launch(gemm_splitk_kernel<2, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
+    else launch(gemm_splitk_kernel<1, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
+}
+
+template <int EPI>
+static void launch_splitk_epi(int ct, dim3 grid, bool two, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
+                              hipStream_t s) {
+    if (ct == 4) launch_splitk_ct<EPI, 4>(grid, two, a, part, ctr, ksplit, s);
+    else if (ct == 3) launch_splitk_ct<EPI, 3>(grid, two, a, part, ctr, ksplit, s);
+    else launch_splitk_ct<EPI, 2>(grid, two, a, part, ctr, ksplit, s);
+}
+
+hipError_t launch_gemm_splitk(int epi, int ct, int ksplit, const GemmArgs& a, float* part, unsigned* ctr,
+                              hipStream_t s) {
+    if (!gemm_splitk_supported(epi, a.M, ct) || a.W2 || ksplit < 1 || ksplit > SPLITK_MAX) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((a.n_tiles + ct - 1) / ct), (unsigned)ksplit);
+    const bool two = a.M > 16;
+    if (epi == EPI_RESID) launch_splitk_epi<EPI_RESID>(ct, grid, two, a, part, ctr, ksplit, s);
+    else if (epi == EPI_QKV) launch_splitk_epi<EPI_QKV>(ct, grid, two, a, part, ctr, ksplit, s);
+    else launch_splitk_epi<EPI_SWIGLU>(ct, grid, two, a, part, ctr, ksplit, s);
+    return hipGetLastError();
+}
+
+// =====================================================================================
 // Tiled GEMM for many rows (M > 64), where the projections approach the MFMA ridge: a
 // workgroup computes a 128-row x 128-column output tile over the whole reduction, so the
 // weights stream once per 128 rows and the operand once per 128 columns.  Per stage of

@@ -236,6 +236,15 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // With a.W2 set (EPI_RESID only) the reduction continues over the second source.
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
+// Split-K GEMM (EPI_RESID, EPI_QKV or EPI_SWIGLU; M <= 32, no second source): ct column
+// tiles per workgroup (2..4), the reduction cut into ksplit slices (1..SPLITK_MAX) whose
+// partials meet in `part` (ceil(n_tiles/ct) * ksplit * 16*ct*ceil(M/16) floats); `ctr`
+// holds one counter per column group, zero before the launch and zero again after it.
+// The normed epilogues take the per-row RMSNorm scale from part_ss as the other GEMMs do.
+constexpr int SPLITK_MAX = 8;
+bool gemm_splitk_supported(int epi, int M, int ct);
+hipError_t launch_gemm_splitk(int epi, int ct, int ksplit, const GemmArgs& a, float* part, unsigned* ctr,
+                              hipStream_t s);
 // Tiled GEMM for M > 64 (no second source): 128 x 128 output tiles.  Needs K % 32 == 0, an
 // even k-step count and the A operand allocated for rows up to a multiple of
 // gemm_tile_row_pad().  gemm_tile_parts gives the number of column groups (the argmax

@@ -398,3 +398,49 @@ def test_8b_layer_batched_block_pass(R, layer8b_b4, mode):
             assert rel_err(O.bf16_bits_to_float(kg[b:b + 1]), nk[0][b:b + 1]) < TOL
             assert rel_err(O.bf16_bits_to_float(vg[b:b + 1]), nv[0][b:b + 1]) < TOL
     assert R.read_device_status(ws) == 0
+
+
+# ----------------------------------------------------------------------------- split-K residual GEMM
+@pytest.mark.parametrize("ksplit,ct", [(1, 4), (2, 2), (3, 4), (8, 4), (8, 2)])
+def test_tiny_split_k_residual_gemm(R, tiny, monkeypatch, ksplit, ct):
+    """QKV, O and down projections cut into ksplit K slices (ragged: the tiny down projection has 22
+    k-steps, so 8 slices of 3 leave the last one a single step and some wavefronts none) of ct column
+    tiles, the slices meeting through the last-arriving workgroup; verify and draft passes against the
+    oracle."""
+    t = tiny
+    monkeypatch.setenv("NLD_SPLITK", str(ksplit))
+    monkeypatch.setenv("NLD_SPLITK_CT", str(ct))
+    ws = R.Workspace(t["model"], 1, 8, 256)
+    for mode in (O.VERIFY, O.DRAFT):
+        ref, _, _ = O.block_forward(t["w"], t["okv"], t["block"], mode)
+        logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(t["block"]).cuda(),
+                                     R.VERIFY if mode == O.VERIFY else R.DRAFT)
+        g = logits.cpu().numpy()
+        e = rel_err(g, ref)
+        log("tiny split-K ksplit=%d ct=%d %s: rel err %.3e" % (ksplit, ct, mode, e))
+        assert e <= TOL
+        check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+    assert R.read_device_status(ws) == 0
+
+
+@pytest.mark.parametrize("k,qkv", [(16, ""), (32, ""), (16, "4,2"), (32, "3,3")])
+def test_8b_layer_split_k_repeatable(R, layer8b, monkeypatch, k, qkv):
+    """The split-K projections' result does not depend on which workgroup arrives last: ten verify
+    passes over the same block give bit-identical logits (a partial read before it was visible
+    would change them), within tolerance of the oracle.  `qkv` also puts the QKV projection on
+    the split-K kernel (ct tiles, ksplit slices)."""
+    if qkv:
+        monkeypatch.setenv("NLD_SPLITK_QKV", qkv)
+    t = layer8b
+    shape = t["shape"]
+    tok = synth_tokens(shape, t["seed"], "8b_layer.block%d" % k, (1, k))
+    ref, _, _ = O.block_forward(t["w"], t["okv"], tok, O.VERIFY)
+    ws = R.Workspace(t["model"], 1, k, t["cache"].max_len)
+    tt = torch.from_numpy(tok).cuda()
+    first, _ = R.block_forward(t["model"], t["cache"], ws, tt, R.VERIFY)
+    first = first.cpu().numpy()
+    assert rel_err(first, ref) <= TOL
+    for i in range(9):
+        again, _ = R.block_forward(t["model"], t["cache"], ws, tt, R.VERIFY)
+        assert np.array_equal(again.cpu().numpy(), first), "pass %d differs" % (i + 1)
+    assert R.read_device_status(ws) == 0
