@@ -192,7 +192,7 @@ class OracleKV:
 # ----------------------------------------------------------------------------- one block forward
 def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode: str,
                   bidir_from: int = 0, positions: np.ndarray | None = None,
-                  rows_for_logits=None):
+                  rows_for_logits=None, block_vis: np.ndarray | None = None):
     """One forward pass of a k-token block per sequence against the cached prefix.
 
     tokens: int [batch, k].  Returns (logits [batch, k, vocab], new_k, new_v)
@@ -201,6 +201,9 @@ def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode
     to commit is decided by acceptance).  ``positions`` overrides the default
     block positions P_b + j.  ``rows_for_logits`` (optional list of row
     indices) restricts the LM head to those rows; other rows get NaN.
+    ``block_vis`` (bool [k, k]) overrides which block columns each block row
+    sees (every row still sees the whole prefix); the LoRA adapter then takes
+    no part (it belongs to the draft pass).
     """
     s = weights.shape
     dt = weights.dtype
@@ -227,7 +230,10 @@ def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode
         o = np.zeros((B, k, s.n_q_heads, s.head_dim), dtype=dt)
         for b in range(B):
             p_b = int(kv.lengths[b])
-            vis = block_visibility(p_b, k, mode, bidir_from)
+            if block_vis is None:
+                vis = block_visibility(p_b, k, mode, bidir_from)
+            else:
+                vis = np.concatenate([np.ones((k, p_b), dtype=bool), np.asarray(block_vis, dtype=bool)], axis=1)
             for g in range(s.n_kv_heads):
                 keys = np.concatenate([kv.k[l][b, g, :p_b], kb[b, :, g]], axis=0)
                 vals = np.concatenate([kv.v[l][b, g, :p_b], vb[b, :, g]], axis=0)
@@ -235,7 +241,7 @@ def block_forward(weights: OracleWeights, kv: OracleKV, tokens: np.ndarray, mode
                     o[b, :, hq] = softmax_attention(q[b, :, hq], keys, vals, vis)
         o2 = o.reshape(B, k, s.q_dim)
         x = x + o2 @ w["wo"].T
-        if mode == DRAFT and "lora_a" in w:
+        if mode == DRAFT and block_vis is None and "lora_a" in w:
             x = x + lora_scale(s) * ((o2 @ w["lora_a"].T) @ w["lora_b"].T)
 
         h = rms_norm(x, w["ffn_norm"], s.rms_eps)
@@ -494,3 +500,126 @@ def diffusion_block(weights, kv, anchor, k: int, threshold: float, bidir_from: i
         block = denoise_step(weights, kv, block, threshold, bidir_from)["block"]
         steps += 1
     return block, steps, refresh(weights, kv, block)
+
+
+# ----------------------------------------------------------------------------- quadratic self-speculation
+# Quadratic self-speculation (Sec. 3.4, Appendix C): one forward pass verifies the
+# previous step's speculative tokens causally, as Mode 3's verify pass does, and in
+# the same pass drafts the next ones for every possible acceptance length (a group of
+# mask tokens after each element of the verified chain, bidirectional within the
+# group), with an optional AR-diffusion ensemble verifier.
+#
+# Readings (the appendix's indices do not close; these keep Mode 3's conventions):
+#
+# * The chain is Mode 3's verify block [anchor, s_1 .. s_{k-1}] (the anchor at
+#   position P).  After chain element c (position P + c) come k mask tokens at
+#   positions P + c + 1 .. P + c + k -- one group per chain element, so that fresh
+#   drafts exist for every acceptance length 0 .. k-1.  Block rows: the chain first,
+#   then mask r (1..k) of group c at row k + c*k + r - 1; k(k+1) rows in all.
+# * Attention: every row sees the cached prefix; chain row c sees chain elements
+#   0..c (causal); a mask of group c sees chain elements 0..c and every mask of its
+#   own group (bidirectional within the group), nothing else.
+# * Predictions: chain row c is AR (it predicts position P + c + 1); mask r of group
+#   c predicts the token at its own position P + c + r, as Mode 3's draft rows do.
+# * The verifier of the token at position P + i (i = 1..k) mixes the AR distribution
+#   of chain row i - 1 with the diffusion distribution of mask 1 of group i - 1 (the
+#   mask at that same position): lambda * p_AR + (1 - lambda) * p_diff; v_i is its
+#   argmax (lowest index on ties).  lambda = 1 is plain AR verification.
+# * Acceptance as in Mode 3: L = longest prefix of s_1..s_{k-1} with s_i = v_i.  The
+#   chain rows 0..L (anchor and accepted tokens) are committed, the next anchor is
+#   v_{L+1}, and the next speculative tokens are the argmax of masks 2..k of group L
+#   (positions P + L + 2 .. P + L + k, right after the next anchor).
+# * The LoRA adapter (a draft-pass feature) is not used by this pass.
+# * The first step's speculative tokens come from a Mode 3 draft pass.
+def quad_rows(k: int) -> int:
+    """Block rows of a quadratic pass with chain length k: k chain rows + k groups of k masks."""
+    return k * (k + 1)
+
+
+def quad_layout(k: int):
+    """Per block row: (position offset from P, group, is_chain).  Group of a chain row c is c."""
+    off, grp, chain = [], [], []
+    for c in range(k):
+        off.append(c)
+        grp.append(c)
+        chain.append(True)
+    for c in range(k):
+        for r in range(1, k + 1):
+            off.append(c + r)
+            grp.append(c)
+            chain.append(False)
+    return np.asarray(off), np.asarray(grp), np.asarray(chain)
+
+
+def quad_block_visibility(k: int) -> np.ndarray:
+    """bool [R, R]: which block columns each block row of the quadratic layout sees."""
+    off, grp, chain = quad_layout(k)
+    R = quad_rows(k)
+    vis = np.zeros((R, R), dtype=bool)
+    for i in range(R):
+        for j in range(R):
+            if chain[j]:
+                vis[i, j] = j <= grp[i]                        # chain columns 0..c (chain row c: causal)
+            else:
+                vis[i, j] = (not chain[i]) and grp[j] == grp[i]   # the own group's masks
+    return vis
+
+
+def quad_tokens(anchor: np.ndarray, spec: np.ndarray, k: int, mask_id: int) -> np.ndarray:
+    """[anchor, s_1 .. s_{k-1}, mask x k^2] per sequence."""
+    B = len(anchor)
+    if np.shape(spec) != (B, k - 1):
+        raise ValueError("spec must hold k-1 tokens per sequence")
+    t = np.full((B, quad_rows(k)), mask_id, dtype=np.int32)
+    t[:, :k] = verify_block(anchor, spec)
+    return t
+
+
+def quad_forward(weights, kv, anchor, spec, k):
+    """The quadratic pass.  Returns (logits [B, R, V], new_k, new_v) with the block's rows in layout order."""
+    off, _, _ = quad_layout(k)
+    positions = kv.lengths[:, None] + off[None, :]
+    return block_forward(weights, kv, quad_tokens(anchor, spec, k, weights.shape.mask_token_id), VERIFY,
+                         positions=positions, block_vis=quad_block_visibility(k))
+
+
+def softmax64(z: np.ndarray) -> np.ndarray:
+    z = np.asarray(z, dtype=np.float64)
+    e = np.exp(z - np.max(z, axis=-1, keepdims=True))
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def ensemble_argmax(ar_logits: np.ndarray, diff_logits: np.ndarray, lam: float) -> np.ndarray:
+    """argmax of lambda * softmax(AR) + (1 - lambda) * softmax(diffusion) over the last axis (float64,
+    first index of the maximum)."""
+    p = lam * softmax64(ar_logits) + (1.0 - lam) * softmax64(diff_logits)
+    return np.argmax(p, axis=-1).astype(np.int32)
+
+
+def quad_verifier(logits: np.ndarray, k: int, lam: float) -> np.ndarray:
+    """v [B, k]: v[:, i-1] is the verifier's token for position P + i, i = 1..k."""
+    ar = logits[:, 0:k]                                 # chain rows 0..k-1
+    diff = logits[:, [k + c * k for c in range(k)]]     # mask 1 of groups 0..k-1
+    return ensemble_argmax(ar, diff, lam)
+
+
+def quad_step(weights, kv, anchor, spec, k: int, lam: float = 1.0):
+    """One quadratic self-speculation step; commits the accepted chain rows into ``kv``.
+
+    spec: int [B, k-1], the previous step's speculative tokens.  Returns dict with the logits,
+    verifier tokens v, accept lengths L, committed tokens, next anchors and next speculative tokens."""
+    anchor = np.asarray(anchor, dtype=np.int32)
+    spec = np.asarray(spec, dtype=np.int32)
+    logits, nk, nv = quad_forward(weights, kv, anchor, spec, k)
+    v = quad_verifier(logits, k, lam)
+    am = argmax_first(logits)
+    Ls, committed, nxt, nspec = [], [], [], []
+    for b in range(len(anchor)):
+        L, c, bonus = accept(spec[b], v[b])
+        Ls.append(L)
+        committed.append(c)
+        nxt.append(bonus)
+        nspec.append(am[b, [k + L * k + r - 1 for r in range(2, k + 1)]])
+    commit(kv, nk, nv, np.asarray(Ls) + 1)
+    return {"logits": logits, "v": v, "L": np.asarray(Ls, dtype=np.int32), "committed": committed,
+            "next_anchor": np.asarray(nxt, dtype=np.int32), "next_spec": np.asarray(nspec, dtype=np.int32).reshape(len(anchor), k - 1)}

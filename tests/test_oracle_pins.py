@@ -553,3 +553,140 @@ def test_lora_draft_equals_full_recompute(lora_mini):
     seq = np.concatenate([prefix, block], axis=1)
     full = O.full_forward(w, seq, O.sequence_visibility(P, k, O.DRAFT), lora_rows=np.arange(P + k) >= P)
     np.testing.assert_allclose(got, full[:, P:], rtol=1e-10, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- quadratic self-speculation
+def test_quad_layout_hand_example():
+    """The quadratic layout for chain length k = 2 (Sec. 3.4, Appendix C, in this build's reading):
+    rows [anchor, s_1, g0.m1, g0.m2, g1.m1, g1.m2] at offsets [0, 1, 1, 2, 2, 3] from P; chain rows are
+    causal, a mask sees the chain up to its group's element and its own group."""
+    off, grp, chain = O.quad_layout(2)
+    assert O.quad_rows(2) == 6
+    assert off.tolist() == [0, 1, 1, 2, 2, 3]
+    assert grp.tolist() == [0, 1, 0, 0, 1, 1]
+    assert chain.tolist() == [True, True, False, False, False, False]
+    expected = np.array([[1, 0, 0, 0, 0, 0],
+                         [1, 1, 0, 0, 0, 0],
+                         [1, 0, 1, 1, 0, 0],
+                         [1, 0, 1, 1, 0, 0],
+                         [1, 1, 0, 0, 1, 1],
+                         [1, 1, 0, 0, 1, 1]], dtype=bool)
+    np.testing.assert_array_equal(O.quad_block_visibility(2), expected)
+
+
+@pytest.fixture(scope="module")
+def quad_mini():
+    w = mini_weights(seed=13)
+    prefix = synth_tokens(MINI, 13, "pin.quad.prefix", (2, 11))
+    spec = synth_tokens(MINI, 13, "pin.quad.spec", (2, 3))
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    return w, kv, prefix[:, -1].copy(), spec, prefix[:, :-1]
+
+
+def test_quad_chain_rows_equal_the_verify_pass(quad_mini):
+    """The chain rows of a quadratic pass are Mode 3's verify pass over [anchor, s_1 .. s_{k-1}]: same
+    logits and same K/V rows (the masks after them are invisible to them)."""
+    w, kv, anchor, spec, _ = quad_mini
+    k = 4
+    logits, nk, nv = O.quad_forward(w, kv, anchor, spec, k)
+    _, vlogits, vk, vv = O.verify_pass(w, kv, anchor, spec)
+    np.testing.assert_allclose(logits[:, :k], vlogits, rtol=1e-10, atol=1e-12)
+    for l in range(MINI.n_layers):
+        np.testing.assert_allclose(nk[l][:, :, :k], vk[l], rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(nv[l][:, :, :k], vv[l], rtol=1e-10, atol=1e-12)
+
+
+def test_quad_groups_equal_draft_passes(quad_mini):
+    """Group c of a quadratic pass is Mode 3's draft pass over [chain_0 .. chain_c, mask x k] with the chain
+    rows causal (bidir_from = c + 1): the same positions, keys and mask, so the same logits."""
+    w, kv, anchor, spec, _ = quad_mini
+    k = 4
+    logits, _, _ = O.quad_forward(w, kv, anchor, spec, k)
+    chain = O.verify_block(anchor, spec)
+    for c in range(k):
+        blk = np.concatenate([chain[:, :c + 1], np.full((2, k), MINI.mask_token_id, dtype=np.int32)], axis=1)
+        dl, _, _ = O.block_forward(w, kv, blk, O.DRAFT, bidir_from=c + 1)
+        rows = [k + c * k + r for r in range(k)]
+        np.testing.assert_allclose(logits[:, rows], dl[:, c + 1:], rtol=1e-10, atol=1e-12)
+
+
+def test_quad_equals_full_recompute(quad_mini):
+    """The cached quadratic pass equals recomputing [prefix ; quadratic block] from tokens with the explicit
+    mask (prefix causal, block rows as the layout says) and the layout's positions."""
+    w, kv, anchor, spec, prefix = quad_mini
+    k = 3
+    spec = spec[:, :k - 1]
+    logits, _, _ = O.quad_forward(w, kv, anchor, spec, k)
+    P = int(kv.lengths[0])
+    R = O.quad_rows(k)
+    toks = np.concatenate([prefix, O.quad_tokens(anchor, spec, k, MINI.mask_token_id)], axis=1)
+    vis = np.tril(np.ones((P + R, P + R), dtype=bool))
+    vis[P:, P:] = O.quad_block_visibility(k)
+    off, _, _ = O.quad_layout(k)
+    pos = np.broadcast_to(np.concatenate([np.arange(P), P + off]), (2, P + R))
+    full = O.full_forward(w, toks, vis, positions=pos)
+    np.testing.assert_allclose(logits, full[:, P:], rtol=1e-10, atol=1e-12)
+
+
+def test_ensemble_argmax_closed_forms():
+    """lambda = 1 is the AR argmax, lambda = 0 the diffusion argmax; a two-token example by hand:
+    p_AR = (0.7, 0.3), p_diff = (0.2, 0.8) mix to (0.45, 0.55) at lambda = 0.5 and (0.55, 0.45) at 0.7;
+    equal mixtures tie to the lower index."""
+    rng = np.random.default_rng(3)
+    a, d = rng.standard_normal((5, 40)), rng.standard_normal((5, 40))
+    np.testing.assert_array_equal(O.ensemble_argmax(a, d, 1.0), O.argmax_first(a))
+    np.testing.assert_array_equal(O.ensemble_argmax(a, d, 0.0), O.argmax_first(d))
+    la, ld = np.log([[0.7, 0.3]]), np.log([[0.2, 0.8]])
+    assert O.ensemble_argmax(la, ld, 0.5)[0] == 1
+    assert O.ensemble_argmax(la, ld, 0.7)[0] == 0
+    assert O.ensemble_argmax(np.log([[0.5, 0.5]]), np.log([[0.5, 0.5]]), 0.3)[0] == 0
+
+
+def test_quad_self_speculation_reproduces_greedy_ar():
+    """With the AR verifier (lambda = 1), quadratic self-speculation commits exactly the greedy AR
+    continuation and builds the same cache, whatever its speculative tokens were."""
+    w = mini_weights(seed=14)
+    prefix = synth_tokens(MINI, 14, "pin.qss.prefix", (2, 9))
+    k, steps = 4, 5
+    kv_q = prefilled(w, prefix[:, :-1], capacity=64)
+    kv_ar = kv_q.copy()
+    anchor = prefix[:, -1].copy()
+    spec, _ = O.draft_pass(w, kv_q, anchor, k)            # the first speculative tokens: a Mode 3 draft
+    out = [[] for _ in range(2)]
+    for _ in range(steps):
+        r = O.quad_step(w, kv_q, anchor, spec, k, lam=1.0)
+        for b in range(2):
+            assert 0 <= r["L"][b] <= k - 1
+            out[b] += r["committed"][b][:-1]               # anchor's successors up to the bonus
+            out[b].append(r["committed"][b][-1])
+        anchor, spec = r["next_anchor"], r["next_spec"]
+    n = min(len(o) for o in out)
+    tok = prefix[:, -1].copy()
+    ar = [[] for _ in range(2)]
+    for _ in range(n):
+        tok, _ = O.ar_step(w, kv_ar, tok)
+        for b in range(2):
+            ar[b].append(int(tok[b]))
+    for b in range(2):
+        assert out[b][:n] == ar[b]
+    m = int(min(kv_q.lengths))
+    for l in range(MINI.n_layers):
+        np.testing.assert_allclose(kv_q.k[l][:, :, :m], kv_ar.k[l][:, :, :m], rtol=1e-9, atol=1e-11)
+
+
+def test_quad_planted_spec_fully_accepted():
+    """Speculative tokens equal to the greedy AR continuation are accepted in full (L = k - 1); the next
+    anchor is the next greedy token and the next speculative tokens come from the last group's masks."""
+    w = mini_weights(seed=15)
+    prefix = synth_tokens(MINI, 15, "pin.qplant.prefix", (1, 9))
+    k = 4
+    kv = prefilled(w, prefix[:, :-1], capacity=64)
+    kv_ar = kv.copy()
+    tok, greedy = prefix[:, -1].copy(), []
+    for _ in range(k):
+        tok, _ = O.ar_step(w, kv_ar, tok)
+        greedy.append(int(tok[0]))
+    r = O.quad_step(w, kv, prefix[:, -1], np.array([greedy[:k - 1]]), k, lam=1.0)
+    assert r["L"][0] == k - 1 and r["committed"][0] == greedy and r["next_anchor"][0] == greedy[-1]
+    am = O.argmax_first(r["logits"])
+    assert r["next_spec"][0].tolist() == [int(am[0, k + (k - 1) * k + i]) for i in range(1, k)]
