@@ -13,7 +13,10 @@ value = block tokens pushed through block-decode passes per second
 Also timed (not part of value), each replayed from its own captured graph:
 "mode2" -- one Mode 2 denoising step over [anchor, mask x (k-1)] at threshold
 0.9 and one K/V refresh of a completed block; "lora_draft" -- a draft pass with
-and without the LoRA-enhanced drafter's adapter (rank 128) on the O projection.
+and without the LoRA-enhanced drafter's adapter (rank 128) on the O projection;
+"quad_ss" -- one quadratic self-speculation step (chain length 7, 56 block rows)
+with the AR verifier and with the lambda = 0.5 ensemble, beside one linear step
+(draft + verify) of the same speculative width.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -134,6 +137,43 @@ def lora_timing(R, model, cache, ws, anchor, k, reps, wl):
            "lora_draft": graph_ms(lambda: R.draft(lmodel, cache, lws, anchor, k, out=d), reps)}
     res["status"] = R.read_device_status(lws)
     lmodel.close()
+    return res
+
+
+QUAD_K = 7   # chain length of the quadratic layout: k(k+1) = 56 block rows per sequence
+
+
+def quad_timing(R, model, cache, anchor, reps):
+    """Mean ms of one quadratic self-speculation step (chain length QUAD_K; AR verifier and the lambda = 0.5
+    ensemble) and of one linear step (draft + verify) at the same speculative width, each replayed from a
+    captured graph with the lengths reset first, so that every replay runs over the same prefix."""
+    import torch
+    k, B, dev = QUAD_K, anchor.shape[0], anchor.device
+    qws = R.QuadWorkspace(model, B, k, cache.max_len)
+    lws = R.Workspace(model, B, k, cache.max_len)
+    a0 = anchor.clone()
+    spec0 = torch.empty((B, k - 1), dtype=torch.int32, device=dev)
+    R.draft(model, cache, lws, a0, k, out=spec0)        # the first speculative tokens: a linear draft
+    len0 = cache.lengths.clone()
+    i32 = lambda *shp: torch.empty(shp, dtype=torch.int32, device=dev)
+    oq = {"accept_len": i32(B), "committed": i32(B, k), "next_anchor": i32(B), "next_spec": i32(B, k - 1)}
+    ol = {"accept_len": i32(B), "committed": i32(B, k), "next_anchor": i32(B)}
+    d = i32(B, k - 1)
+
+    def quad(lam):
+        cache.lengths.copy_(len0)
+        R.quad_step(model, cache, qws, a0, spec0, k, lam, outs=oq)
+
+    def linear():
+        cache.lengths.copy_(len0)
+        R.draft(model, cache, lws, a0, k, out=d)
+        R.verify_accept(model, cache, lws, a0, d, k, outs=ol)
+
+    res = {"quad_ar": graph_ms(lambda: quad(1.0), reps), "quad_ensemble": graph_ms(lambda: quad(0.5), reps),
+           "linear": graph_ms(linear, reps)}
+    res["status"] = R.read_device_status(qws) | R.read_device_status(lws)
+    cache.lengths.copy_(len0)
+    torch.cuda.synchronize()
     return res
 
 
@@ -319,12 +359,13 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
-        m2_ms = lora_ms = None
+        m2_ms = lora_ms = quad_ms = None
         if not args.no_extras:
             block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
             m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
             lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
-            status |= R.read_device_status(ws) | lora_ms["status"]
+            quad_ms = quad_timing(R, model, cache, anchor, max(5, steps // 2))
+            status |= R.read_device_status(ws) | lora_ms["status"] | quad_ms["status"]
 
     ms_per_step = elapsed_ms / steps
     value = 2.0 * B * k / (ms_per_step * 1e-3)
@@ -388,6 +429,16 @@ def main():
             "lora_draft_hbm_frac": round((pass_bytes(shape, B, k, plens) + shape.n_layers * 2 * LORA_RANK
                                           * (shape.q_dim + shape.hidden)) / (lora_ms["lora_draft"] * 1e-3) / 1e9
                                          / HBM_PEAK_GBS, 4),
+        }
+    if quad_ms is not None:
+        R_q = QUAD_K * (QUAD_K + 1)
+        res["quad_ss"] = {
+            "k": QUAD_K, "block_rows": R_q,
+            "step_ms_ar_verifier": round(quad_ms["quad_ar"], 4),
+            "step_ms_ensemble_lambda_0.5": round(quad_ms["quad_ensemble"], 4),
+            "linear_step_ms_same_width": round(quad_ms["linear"], 4),
+            "quad_hbm_frac": round(pass_bytes(shape, B, R_q, plens) / (quad_ms["quad_ar"] * 1e-3) / 1e9
+                                   / HBM_PEAK_GBS, 4),
         }
     if not args.no_cpu_baseline:
         del model, cache, ws

@@ -253,6 +253,39 @@ nld_status nld_decode_steps(const nld_model* m, const nld_kv_cache* kv, int32_t*
  * for non-positive times or k_ss < 2. */
 int32_t nld_choose_block(float ar_step_ms, float ss_step_ms, float expected_committed, int32_t k_ss);
 
+/* ---- quadratic self-speculation (Sec. 3.4, Appendix C) -------------------------
+ * One forward pass that both verifies the previous step's speculative tokens and
+ * drafts the next ones for every possible acceptance length.  The block of each
+ * sequence is the chain [anchor, s_1 .. s_{k-1}] (Mode 3's verify block: chain
+ * element c at position P_b + c) followed by one group of k mask tokens per chain
+ * element (mask r = 1..k of group c at position P_b + c + r): k(k+1) rows.  Every
+ * row sees the cached prefix; chain row c sees chain elements 0..c; a mask of
+ * group c sees chain elements 0..c and its own group's masks.  Chain rows predict
+ * the next position (AR); masks predict their own position (diffusion).
+ * Verifier token v_i of position P_b + i (i = 1..k): argmax of
+ * lambda * softmax(chain row i-1) + (1 - lambda) * softmax(mask 1 of group i-1),
+ * lowest index on ties (lambda = 1: AR verification; 0: diffusion).  Then
+ * Mode 3's acceptance: L = longest prefix with s_i = v_i, committed[b] =
+ * s_1..s_L, v_{L+1}, -1 padded to k; lengths[b] += L+1 (the chain rows' K/V,
+ * written to cache rows [P_b, P_b + k), become committed); next_anchor[b] =
+ * v_{L+1}; next_spec[b][r-2] = argmax of mask r of group L, r = 2..k (the tokens
+ * at positions P_b + L + 2 .. P_b + L + k, right after the next anchor).
+ * spec / next_spec int32 [batch][k-1] (next_spec may alias spec, next_anchor may
+ * alias anchor); accept_len [batch]; committed [batch][k]; logits (optional) f32
+ * [batch][k(k+1)][vocab] in block-row order.  The first step's speculative
+ * tokens come from nld_draft.  The LoRA adapter is not used by this pass.
+ * The workspace must hold nld_quad_workspace_bytes(m, batch, k, max_len)
+ * (initialized with nld_workspace_init).
+ * Errors: INVALID_ARG (k outside [2, NLD_QUAD_MAX_K], lambda outside [0, 1] or
+ * NaN, a NULL pointer, and the checks of nld_block_forward for k(k+1) rows),
+ * SHAPE ((n_q_heads/n_kv_heads) * k(k+1) > 256), CAPACITY (workspace). */
+#define NLD_QUAD_MAX_K 7   /* k(k+1) block rows must fit one 64-key stage of the block attention */
+size_t nld_quad_workspace_bytes(const nld_model* m, int32_t batch, int32_t k, int32_t max_len);
+nld_status nld_quad_step(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor, const int32_t* spec,
+                         int32_t batch, int32_t k, float lambda, int32_t* accept_len, int32_t* committed,
+                         int32_t* next_anchor, int32_t* next_spec, float* logits, void* workspace, size_t ws_bytes,
+                         void* stream);
+
 /* ---- Mode 2: block-wise diffusion denoising (Sec. 3.2) -----------------------
  * Confidence-based decoding of one block per sequence: the block starts as
  * [anchor, mask x (k-1)] and each denoising step, one diffusion (draft) pass

@@ -33,7 +33,7 @@ EXPORTED = [
     "nld_pack_linear", "nld_pack_qkv", "nld_pack_gate_up", "nld_workspace_bytes", "nld_workspace_init",
     "nld_block_forward", "nld_draft", "nld_verify_accept", "nld_accept_workspace_bytes",
     "nld_accept_from_logits", "nld_denoise_step", "nld_refresh_block", "nld_commit_from_logits",
-    "nld_decode_steps", "nld_choose_block",
+    "nld_decode_steps", "nld_choose_block", "nld_quad_workspace_bytes", "nld_quad_step",
     "nld_read_device_status", "nld_trace_enable", "nld_trace_read",
 ]
 
@@ -117,6 +117,11 @@ def load():
     L.nld_accept_workspace_bytes.argtypes = [c_i32, c_i32]
     L.nld_accept_from_logits.restype = c_i32
     L.nld_accept_from_logits.argtypes = [c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.nld_quad_workspace_bytes.restype = c_sz
+    L.nld_quad_workspace_bytes.argtypes = [c_vp, c_i32, c_i32, c_i32]
+    L.nld_quad_step.restype = c_i32
+    L.nld_quad_step.argtypes = [c_vp, P(KVCache), c_vp, c_vp, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                c_sz, c_vp]
     L.nld_denoise_step.restype = c_i32
     L.nld_denoise_step.argtypes = [c_vp, P(KVCache), c_vp, c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                    c_sz, c_vp]

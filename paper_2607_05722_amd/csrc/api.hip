@@ -97,10 +97,12 @@ struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
     int n_sk_ctr, sk_ctr0;   // split-K residual GEMM: counters (one per column group) from tile counter sk_ctr0
     size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, sk_part, lora_t, drafts,
-        total;
+        ens_logits, ens_v, total;
 };
 
-Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
+// k: block rows per sequence.  quad_k > 0: the block is a quadratic self-speculation layout
+// with chain length quad_k (k = quad_k * (quad_k + 1)), which adds the ensemble verifier's buffers.
+Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_k = 0) {
     Layout L{};
     L.M = batch * k;
     // operand rows: whole 64-row groups, or whole 128-row tiles of the tiled GEMM (M > 64)
@@ -161,6 +163,9 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len) {
     L.blk_v = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);
     L.lora_t = take(4 * (size_t)L.Mpad * c.lora_rank);   // split lora_scale * (A o), draft passes only
     L.drafts = take(4 * (size_t)batch * k);              // nld_decode_steps: one step's drafts
+    // quadratic self-speculation: the verifier rows' logits [batch][2 quad_k][vocab] and tokens [batch][quad_k]
+    L.ens_logits = take(4 * (size_t)batch * 2 * quad_k * c.vocab);
+    L.ens_v = take(4 * (size_t)batch * quad_k);
     L.total = off;
     return L;
 }
@@ -250,7 +255,7 @@ StreamPlan plan_stream(int epi, int M, int n_tiles) {
     return p;
 }
 
-enum Source { SRC_TOKENS = 0, SRC_DRAFT = 1, SRC_VERIFY = 2 };
+enum Source { SRC_TOKENS = 0, SRC_DRAFT = 1, SRC_VERIFY = 2, SRC_QUAD = 3 };
 
 struct PassIO {
     int source;
@@ -273,10 +278,16 @@ struct PassIO {
     int32_t* n_masked;
     float* conf_out;
     bool kv_only;   // refresh: stop after the last layer's K/V (no attention, FFN or LM head after it)
+    // quadratic self-speculation (mode NLD_MODE_QUAD_INTERNAL): chain length and the verifier's mixture
+    int quad_k;
+    float lambda;
 };
 
+// Attention mode of a quadratic pass (never a caller's mode value).
+constexpr int NLD_MODE_QUAD_INTERNAL = 2;
+
 nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, int k, void* ws, size_t ws_bytes,
-                         Layout* out) {
+                         Layout* out, int quad_k = 0) {
     if (!m) return fail(NLD_ERR_INVALID_ARG, "model is NULL");
     if (!kv || !kv->k || !kv->v || !kv->lengths) return fail(NLD_ERR_INVALID_ARG, "kv cache or one of its pointers is NULL");
     if (!ws) return fail(NLD_ERR_INVALID_ARG, "workspace is NULL");
@@ -287,7 +298,7 @@ nld_status validate_call(const nld_model* m, const nld_kv_cache* kv, int batch, 
     const nld_config& c = m->cfg;
     const int G = c.n_q_heads / c.n_kv_heads;
     if (G * k > 256) return fail(NLD_ERR_SHAPE, "(n_q_heads/n_kv_heads)*k = %d exceeds 256", G * k);
-    *out = make_layout(c, batch, k, kv->max_len);
+    *out = make_layout(c, batch, k, kv->max_len, quad_k);
     if (ws_bytes < out->total)
         return fail(NLD_ERR_CAPACITY, "workspace holds %zu bytes, this call needs %zu", ws_bytes, out->total);
     return NLD_OK;
@@ -400,6 +411,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.lengths = kv->lengths;
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;
+    e.quad_k = io.quad_k;
     for (int i = 0; i < c.head_dim / 2; ++i) e.inv_freq[i] = pow((double)c.rope_base, -2.0 * i / (double)c.head_dim);
     {
         TraceScope ts(NLD_TRACE_EMBED, s);
@@ -423,7 +435,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.q_row_tiles = L.row_tiles;
         g.kc = kc;
         g.vc = vc;
-        g.write_cache = io.mode == NLD_MODE_VERIFY;
+        g.write_cache = io.mode == NLD_MODE_VERIFY || io.mode == NLD_MODE_QUAD_INTERNAL;   // quad: chain rows
+        g.quad_k = io.quad_k;
         g.blk_k = at<uint16_t>(ws, L.blk_k);
         g.blk_v = at<uint16_t>(ws, L.blk_v);
         g.lengths = kv->lengths;
@@ -461,6 +474,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.bidir_from = io.bidir_from;
         at_.rows_pad = L.rows_pad;
         at_.row_tiles = L.row_tiles;
+        at_.quad_k = io.quad_k;
         at_.n_parts = L.n_parts;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
         {
@@ -554,6 +568,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     }
 
     const bool denoise = io.finish == FINISH_DENOISE;
+    const bool ensemble = io.finish == FINISH_QUAD && io.lambda > 0.0f && io.lambda < 1.0f;
     GemmArgs gl{};
     gl.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * c.n_layers;
     gl.eps = c.rms_eps;
@@ -564,8 +579,11 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     gl.ksteps = ks_h;
     gl.logits = io.logits;
     gl.part_keys = at<unsigned long long>(ws, L.keys);
-    gl.part_lse = denoise ? at<float2>(ws, L.lse) : nullptr;
+    gl.part_lse = (denoise || ensemble) ? at<float2>(ws, L.lse) : nullptr;
     gl.exclude_id = denoise ? c.mask_token_id : -1;
+    gl.k_blk = k;
+    gl.quad_k = io.quad_k;
+    gl.ens_logits = ensemble ? at<float>(ws, L.ens_logits) : nullptr;
     gl.vocab = c.vocab;
     int parts = 0;
     {
@@ -589,6 +607,16 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     fa.committed = io.committed;
     fa.next_anchor = io.next_anchor;
     fa.lengths = io.advance_lengths ? kv->lengths : nullptr;
+    if (io.finish == FINISH_QUAD) {
+        fa.quad_k = io.quad_k;
+        fa.lambda = io.lambda;
+        fa.ens_logits = at<float>(ws, L.ens_logits);
+        fa.ens_v = at<int32_t>(ws, L.ens_v);
+        TraceScope ts(NLD_TRACE_ARGMAX, s);
+        if (ensemble) HIP_TRY(launch_quad_ensemble(fa, s));
+        HIP_TRY(launch_quad_finish(fa, s));
+        return NLD_OK;
+    }
     {
         TraceScope ts(NLD_TRACE_ARGMAX, s);
         HIP_TRY(launch_finish(fa, s));
@@ -782,6 +810,40 @@ nld_status nld_verify_accept(const nld_model* m, const nld_kv_cache* kv, const i
     io.next_anchor = next_anchor;
     io.advance_lengths = true;
     return run_pass(m, kv, batch, k, io, workspace, L, (hipStream_t)stream);
+}
+
+size_t nld_quad_workspace_bytes(const nld_model* m, int32_t batch, int32_t k, int32_t max_len) {
+    if (!m || batch < 1 || k < 2 || k > NLD_QUAD_MAX_K || max_len < 1) return 0;
+    return make_layout(m->cfg, batch, k * (k + 1), max_len, k).total;
+}
+
+nld_status nld_quad_step(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor, const int32_t* spec,
+                         int32_t batch, int32_t k, float lambda, int32_t* accept_len, int32_t* committed,
+                         int32_t* next_anchor, int32_t* next_spec, float* logits, void* workspace, size_t ws_bytes,
+                         void* stream) {
+    if (k < 2 || k > NLD_QUAD_MAX_K) return fail(NLD_ERR_INVALID_ARG, "quadratic k must be in [2, %d] (got %d)",
+                                                 NLD_QUAD_MAX_K, k);
+    if (!(lambda >= 0.0f && lambda <= 1.0f)) return fail(NLD_ERR_INVALID_ARG, "lambda must be in [0, 1]");
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k * (k + 1), workspace, ws_bytes, &L, k);
+    if (st != NLD_OK) return st;
+    if (!anchor || !spec || !accept_len || !committed || !next_anchor || !next_spec)
+        return fail(NLD_ERR_INVALID_ARG, "anchor, spec, accept_len, committed, next_anchor or next_spec is NULL");
+    PassIO io{};
+    io.source = SRC_QUAD;
+    io.anchor = anchor;
+    io.draft_in = spec;
+    io.mode = NLD_MODE_QUAD_INTERNAL;
+    io.logits = logits;
+    io.finish = FINISH_QUAD;
+    io.accept_len = accept_len;
+    io.committed = committed;
+    io.next_anchor = next_anchor;
+    io.draft_out = next_spec;
+    io.advance_lengths = true;
+    io.quad_k = k;
+    io.lambda = lambda;
+    return run_pass(m, kv, batch, k * (k + 1), io, workspace, L, (hipStream_t)stream);
 }
 
 nld_status nld_denoise_step(const nld_model* m, const nld_kv_cache* kv, int32_t* block, int32_t batch, int32_t k,

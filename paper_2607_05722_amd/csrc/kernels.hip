@@ -104,6 +104,7 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, float y, int m, int t
         a.blk_v[((unit * 2 + 1) * D + dim) * 64 + jb] = lo;
     }
     if (!a.write_cache) return;
+    if (a.quad_k > 0 && jb >= a.quad_k) return;   // quadratic layout: only the chain rows are AR rows
     if (pos >= a.max_len) atomicOr(a.status, DEV_CAPACITY);
     else if (kind == 1) a.kc[(unit * a.max_len + pos) * D + dim] = ob;
     else a.vc[((unit * (a.max_len / 64) + pos / 64) * D + dim) * 64 + (pos & 63)] = ob;
@@ -137,6 +138,11 @@ __device__ __forceinline__ unsigned long long epi_lmhead(const GemmArgs& a, floa
     const bool in = m < a.M && n < a.vocab;
     const bool ok = in && n != a.exclude_id;
     if (in && a.logits) a.logits[(size_t)m * a.vocab + n] = y;
+    if (in && a.ens_logits) {   // quadratic layout: the verifier rows (chain row i, mask 1 of group i)
+        const int b = m / a.k_blk, jb = m - b * a.k_blk, qk = a.quad_k;
+        const int ci = jb < qk ? jb : ((jb - qk) % qk == 0 ? qk + (jb - qk) / qk : -1);
+        if (ci >= 0) a.ens_logits[((size_t)b * 2 * qk + ci) * a.vocab + n] = y;
+    }
     unsigned long long key = ok ? argmax_key(y, (uint32_t)n) : 0ull;
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) key = umax64(key, __shfl_xor(key, off));
@@ -1075,7 +1081,14 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const int j = row_ok ? row % k : 0;
 
     const int P_raw = a.lengths[b];   // requested first; the loads below do not depend on it
+    // Block columns this row sees.  Verify: c <= j.  Draft: every column from row bidir_from on.
+    // Quadratic layout (mode 2, chain length qk): chain row j sees chain columns c <= j; a mask of
+    // group grp sees chain columns c <= grp and the columns [lo_c, hi_c) of its own group.
+    const int qk = a.quad_k;
+    const bool quad = a.mode == 2;
     const bool bidir_row = (a.mode == 1) && (j >= a.bidir_from);
+    const int grp = (quad && j >= qk) ? (j - qk) / qk : j;
+    const int lo_c = (quad && j >= qk) ? qk + grp * qk : k, hi_c = (quad && j >= qk) ? lo_c + qk : k;
     const int split_beg = split * a.chunk;   // prefix splits: first key of the split (< max_len)
 
     const size_t head_off = (size_t)(b * nkv + kvh) * a.max_len * D;
@@ -1205,7 +1218,9 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
                 float x = s[tt][i] * a.scale_log2;
                 if (edge) {
                     const int key = kb + stage_key(TPW * kh + tt, 4 * g + i);
-                    const bool vis = key < kend && (key < P || (key - P) <= j || bidir_row);
+                    const int c = key - P;   // block column (keys < P are the prefix)
+                    const bool vis = key < kend && (key < P || (quad ? ((c < qk && c <= grp) || (c >= lo_c && c < hi_c))
+                                                                     : (c <= j || bidir_row)));
                     x = vis ? x : -INFINITY;
                 }
                 sv[tt * 4 + i] = x;
@@ -1409,7 +1424,10 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
     // reduced to [-pi, pi] and evaluated in fp64, stored as fp32 (cos, sin).
     if ((int)threadIdx.x < a.head_dim / 2) {
         const int fi = threadIdx.x;
-        const int pos = committed_length(a.lengths, b, a.max_len, a.status) + j;
+        // quadratic layout: mask r of group c (row qk + c*qk + r - 1) sits at P + c + r
+        const int qk = a.quad_k;
+        const int off = (qk > 0 && j >= qk) ? (j - qk) / qk + (j - qk) % qk + 1 : j;
+        const int pos = committed_length(a.lengths, b, a.max_len, a.status) + off;
         const double two_pi = 6.283185307179586476925286766559;
         double ang = (double)pos * a.inv_freq[fi];
         ang -= two_pi * rint(ang * (1.0 / two_pi));
@@ -1419,6 +1437,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
     if (a.source == 0) tok = a.tokens[m];
     else if (j == 0) tok = a.anchor[b];
     else if (a.source == 1) tok = a.mask_id;
+    else if (a.source == 3) tok = j < a.quad_k ? a.draft[b * (a.quad_k - 1) + j - 1] : a.mask_id;
     else tok = a.draft[b * (a.k_blk - 1) + j - 1];
     if (tok < 0 || tok >= a.vocab) {
         if (threadIdx.x == 0) atomicOr(a.status, DEV_BAD_TOKEN);
@@ -1567,6 +1586,108 @@ __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s) {
     const int threads = a.finish == FINISH_REFRESH ? 64 : 64 * (a.k_blk < 16 ? a.k_blk : 16);
     launch(finish_kernel, dim3(a.batch), dim3(threads), s, a);
+    return hipGetLastError();
+}
+
+// =====================================================================================
+// Quadratic self-speculation (Sec. 3.4, Appendix C).  The block of each sequence is the
+// chain [anchor, s_1 .. s_{qk-1}] followed by qk groups of qk masks (k_blk = qk(qk+1)
+// rows).  The verifier token v_i of position P + i (i = 1..qk) comes from chain row i-1
+// (AR), from mask 1 of group i-1 (diffusion), or from their mixture
+// lambda * softmax(AR) + (1 - lambda) * softmax(diffusion).  Acceptance is Mode 3's; the
+// next speculative tokens are the argmax of masks 2..qk of group L.
+// =====================================================================================
+// argmax of row m from the LM head's per-workgroup keys, in every lane of the wavefront
+__device__ __forceinline__ int32_t row_argmax(const FinishArgs& a, int m, int lane) {
+    const unsigned long long* pk = a.part_keys + (size_t)m * a.n_parts;
+    unsigned long long best = 0ull;
+    for (int p = lane; p < a.n_parts; p += 64) best = umax64(best, pk[p]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) best = umax64(best, __shfl_xor(best, off));
+    return argmax_key_index(best);
+}
+
+// softmax statistics (max, sum of exp(z - max)) of row m, merged over the LM head's
+// workgroups, in every lane of the wavefront
+__device__ __forceinline__ float2 row_lse(const FinishArgs& a, int m, int lane) {
+    float2 st = float2{-INFINITY, 0.f};
+    for (int p = lane; p < a.n_parts; p += 64) st = lse_merge(st, a.part_lse[(size_t)m * a.n_parts + p]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) st = lse_merge(st, float2{__shfl_xor(st.x, off), __shfl_xor(st.y, off)});
+    return st;
+}
+
+// One workgroup per (sequence b, position i): v_{i+1} = argmax over the vocabulary of
+// lambda * exp(a_n - A) / SA + (1 - lambda) * exp(d_n - D) / SD (lowest index on ties).
+__global__ void __launch_bounds__(1024) quad_ensemble_kernel(FinishArgs a) {
+    __shared__ float2 st_s[2];
+    __shared__ unsigned long long key_s[16];
+    const int b = blockIdx.x, i = blockIdx.y, qk = a.quad_k, R = a.k_blk, V = a.vocab;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    if (wave < 2) {
+        const float2 st = row_lse(a, b * R + (wave == 0 ? i : qk + i * qk), lane);
+        if (lane == 0) st_s[wave] = st;
+    }
+    __syncthreads();
+    const float2 sa = st_s[0], sd = st_s[1];
+    const float ca = a.lambda / sa.y, cd = (1.0f - a.lambda) / sd.y;
+    const float* la = a.ens_logits + ((size_t)b * 2 * qk + i) * V;
+    const float* ld = a.ens_logits + ((size_t)b * 2 * qk + qk + i) * V;
+    unsigned long long best = 0ull;
+    for (int n = threadIdx.x; n < V; n += blockDim.x) {
+        const float p = ca * expf(la[n] - sa.x) + cd * expf(ld[n] - sd.x);
+        best = umax64(best, argmax_key(p, (uint32_t)n));
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) best = umax64(best, __shfl_xor(best, off));
+    if (lane == 0) key_s[wave] = best;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long k2 = 0ull;
+        for (int w = 0; w < nw; ++w) k2 = umax64(k2, key_s[w]);
+        a.ens_v[b * qk + i] = argmax_key_index(k2);
+    }
+}
+
+// One workgroup per sequence: verifier tokens, acceptance, commit, next anchor and the next
+// speculative tokens.  draft_out may alias draft_in and next_anchor the anchor the pass read.
+__global__ void __launch_bounds__(1024) quad_finish_kernel(FinishArgs a) {
+    __shared__ int32_t v_s[64];
+    __shared__ int L_s;
+    const int b = blockIdx.x, qk = a.quad_k, R = a.k_blk;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    for (int i = wave; i < qk; i += nw) {
+        int32_t v;
+        if (a.lambda > 0.0f && a.lambda < 1.0f) v = a.ens_v[b * qk + i];
+        else v = row_argmax(a, b * R + (a.lambda >= 1.0f ? i : qk + i * qk), lane);
+        if (lane == 0) v_s[i] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int32_t* sp = a.draft_in + (size_t)b * (qk - 1);
+        int L = 0;
+        while (L < qk - 1 && sp[L] == v_s[L]) ++L;
+        for (int i = 0; i < qk; ++i) a.committed[(size_t)b * qk + i] = i < L ? sp[i] : (i == L ? v_s[L] : -1);
+        a.accept_len[b] = L;
+        a.next_anchor[b] = v_s[L];
+        if (a.lengths) a.lengths[b] += L + 1;
+        L_s = L;
+    }
+    __syncthreads();
+    const int L = L_s;
+    for (int r = 2 + wave; r <= qk; r += nw) {
+        const int32_t v = row_argmax(a, b * R + qk + L * qk + r - 1, lane);
+        if (lane == 0) a.draft_out[(size_t)b * (qk - 1) + r - 2] = v;
+    }
+}
+
+hipError_t launch_quad_ensemble(const FinishArgs& a, hipStream_t s) {
+    launch(quad_ensemble_kernel, dim3(a.batch, a.quad_k), dim3(1024), s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_quad_finish(const FinishArgs& a, hipStream_t s) {
+    launch(quad_finish_kernel, dim3(a.batch), dim3(64 * (a.quad_k < 16 ? a.quad_k : 16)), s, a);
     return hipGetLastError();
 }
 

@@ -132,6 +132,12 @@ struct GemmArgs {
     int exclude_id;                  // column left out of the argmax and the sums (-1: none)
     int n_parts;
     int vocab;
+    // Quadratic self-speculation: quad_k chain rows lead every block of k_blk = quad_k * (quad_k + 1)
+    // rows (then quad_k groups of quad_k masks).  Only chain rows write the cache; the LM head
+    // copies the logits of the verifier rows (chain row i and mask 1 of group i, i < quad_k) to
+    // ens_logits [batch][2 * quad_k][vocab] when that buffer is given.
+    int quad_k;
+    float* ens_logits;
 };
 
 // Queries are stored per (sequence b, KV head) unit with the unit's rows
@@ -154,6 +160,7 @@ struct AttnArgs {
     float* part_ml;      // [units][n_parts][rows_pad][2]
     int k_blk, n_q_heads, n_kv_heads, max_len, n_splits, chunk, mode, bidir_from, rows_pad;
     int row_tiles;       // query-row tiles of 16 per unit (GQA group size x k / 16, rounded up)
+    int quad_k;          // mode 2 (quadratic self-speculation): chain length of the block's layout
     int n_parts;         // partial results per (unit, row): n_splits prefix splits + the block part
     float scale_log2;    // log2(e) / sqrt(D)
 };
@@ -176,10 +183,13 @@ struct EmbedArgs {
     float2* rope;
     const int32_t* lengths;
     int max_len, head_dim;
+    int quad_k;             // source 3: chain length of the quadratic layout (block row positions follow it)
     double inv_freq[64];    // base^(-2i/head_dim), computed on the host in fp64
 };
 
-enum FinishKind { FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2, FINISH_DENOISE = 3, FINISH_REFRESH = 4 };
+enum FinishKind {
+    FINISH_NONE = 0, FINISH_DRAFT = 1, FINISH_ACCEPT = 2, FINISH_DENOISE = 3, FINISH_REFRESH = 4, FINISH_QUAD = 5
+};
 
 struct FinishArgs {
     const unsigned long long* part_keys;  // [M][n_parts] (or NULL: reduce `logits`)
@@ -204,6 +214,14 @@ struct FinishArgs {
     int32_t* n_masked;                    // [batch] masks left after the commit
     float* conf_out;                      // optional [M]
     uint32_t* status;
+    // FINISH_QUAD: chain length quad_k (k_blk = quad_k * (quad_k + 1) rows per sequence); draft_in
+    // holds the speculative tokens [batch][quad_k - 1], draft_out receives the next ones; the
+    // verifier is the AR row (lambda >= 1), the diffusion row (lambda <= 0) or, in between, the
+    // ensemble kernel's tokens in ens_v [batch][quad_k] (from ens_logits and part_lse).
+    int quad_k;
+    float lambda;
+    const float* ens_logits;
+    int32_t* ens_v;
 };
 
 enum PackKind { PACK_LINEAR = 0, PACK_QKV = 1, PACK_GATE_UP = 2 };
@@ -257,5 +275,9 @@ hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s);
+// Quadratic self-speculation: the ensemble verifier's tokens (0 < lambda < 1; grid batch x quad_k),
+// then acceptance, commit and the next speculative tokens (grid batch).
+hipError_t launch_quad_ensemble(const FinishArgs& a, hipStream_t s);
+hipError_t launch_quad_finish(const FinishArgs& a, hipStream_t s);
 
 }  // namespace nld

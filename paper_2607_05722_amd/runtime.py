@@ -229,6 +229,17 @@ class Workspace:
         return _ptr(self.buf)
 
 
+class QuadWorkspace(Workspace):
+    """Workspace of quadratic self-speculation steps with chain length k (k(k+1) block rows)."""
+
+    def __init__(self, model: DeviceModel, batch: int, k: int, max_len: int):
+        lib = C.load()
+        self.nbytes = lib.nld_quad_workspace_bytes(model.handle, batch, k, max_len)
+        assert self.nbytes > 0
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=model.device)
+        C.check(lib.nld_workspace_init(_ptr(self.buf), self.nbytes, stream_handle()))
+
+
 def block_forward(model, cache, ws, tokens: torch.Tensor, mode: int, bidir_from: int = 0, want_logits=True):
     """One block pass.  tokens: int32 [batch][k] on the device.  Returns (logits or None, argmax)."""
     batch, k = tokens.shape
@@ -338,6 +349,27 @@ def decode_steps(model, cache, ws, anchor: torch.Tensor, k: int, n_steps: int, b
                                       bidir_from, _ptr(outs["accept_len"]), _ptr(outs["committed"]), ws.ptr,
                                       ws.nbytes, stream_handle()))
     return outs
+
+
+def quad_step(model, cache, ws, anchor: torch.Tensor, spec: torch.Tensor, k: int, lam: float = 1.0,
+              want_logits=False, outs=None):
+    """One quadratic self-speculation step over [anchor, spec] and k groups of k masks.  Returns dict of
+    device tensors: accept_len, committed [batch][k], next_anchor, next_spec [batch][k-1], logits or None
+    ([batch][k(k+1)][vocab]).  ``outs`` may pass next_anchor=anchor and next_spec=spec to update in place."""
+    batch = anchor.shape[0]
+    dev = model.device
+    o = dict(outs or {})
+    o.setdefault("accept_len", torch.empty(batch, dtype=torch.int32, device=dev))
+    o.setdefault("committed", torch.empty((batch, k), dtype=torch.int32, device=dev))
+    o.setdefault("next_anchor", torch.empty(batch, dtype=torch.int32, device=dev))
+    o.setdefault("next_spec", torch.empty((batch, k - 1), dtype=torch.int32, device=dev))
+    logits = torch.empty((batch, k * (k + 1), model.shape.vocab), dtype=torch.float32, device=dev) \
+        if want_logits else None
+    C.check(C.load().nld_quad_step(model.handle, ctypes.byref(cache.struct), _ptr(anchor), _ptr(spec), batch, k,
+                                   float(lam), _ptr(o["accept_len"]), _ptr(o["committed"]), _ptr(o["next_anchor"]),
+                                   _ptr(o["next_spec"]), _ptr(logits), ws.ptr, ws.nbytes, stream_handle()))
+    o["logits"] = logits
+    return o
 
 
 def choose_block(ar_step_ms: float, ss_step_ms: float, expected_committed: float, k_ss: int) -> int:

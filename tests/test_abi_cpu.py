@@ -190,3 +190,31 @@ def test_choose_block_rule():
     assert lib.nld_choose_block(1.0, 2.0, 2.0, 16) == 1         # a tie keeps AR
     assert lib.nld_choose_block(0.0, 2.0, 9.0, 16) == 1
     assert lib.nld_choose_block(1.0, 2.0, 9.0, 1) == 1
+
+
+def test_quad_step_validation():
+    """Quadratic self-speculation: k in [2, 7], lambda in [0, 1] (not NaN), non-NULL arguments, the
+    quadratic workspace size, and the GQA row limit on k(k+1) block rows."""
+    lib = C.load()
+    st, h, c = fake_model()
+    kv = C.KVCache(0x1000, 0x1000, 0x1000, 1, 256)
+    p = 0x1000
+    need = lib.nld_quad_workspace_bytes(h, 1, 4, 256)
+    assert need > lib.nld_workspace_bytes(h, 1, 20, 256)         # plus the ensemble verifier's buffers
+    assert lib.nld_quad_workspace_bytes(h, 1, 1, 256) == 0
+    assert lib.nld_quad_workspace_bytes(h, 1, 8, 256) == 0
+    args = lambda k=4, lam=0.5, anchor=p, spec=p, ws=need: (h, ctypes.byref(kv), anchor, spec, 1, k, lam, p, p, p, p,
+                                                            None, p, ws, None)
+    assert lib.nld_quad_step(*args(k=1)) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_quad_step(*args(k=8)) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_quad_step(*args(lam=1.5)) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_quad_step(*args(lam=float("nan"))) == C.NLD_ERR_INVALID_ARG
+    assert b"lambda" in lib.nld_last_error()
+    assert lib.nld_quad_step(*args(spec=None)) == C.NLD_ERR_INVALID_ARG
+    assert lib.nld_quad_step(*args(ws=lib.nld_workspace_bytes(h, 1, 20, 256))) == C.NLD_ERR_CAPACITY
+    lib.nld_model_destroy(h)
+    st, h, c = fake_model(n_q_heads=16, n_kv_heads=2)             # 8 x 7 x 8 rows per KV head > 256
+    kv = C.KVCache(0x1000, 0x1000, 0x1000, 1, 256)
+    big = lib.nld_quad_workspace_bytes(h, 1, 7, 256)
+    assert lib.nld_quad_step(h, ctypes.byref(kv), p, p, 1, 7, 1.0, p, p, p, p, None, p, big, None) == C.NLD_ERR_SHAPE
+    lib.nld_model_destroy(h)

@@ -225,3 +225,28 @@ def test_8b_full_lora_draft(R):
     near = check_argmax(d.cpu().numpy(), g[:, 1:], ref[:, 1:], e * np.max(np.abs(ref)))
     log("8b lora: near-tie draft rows differing: %s" % near)
     assert R.read_device_status(ws) == 0
+
+
+def test_8b_full_quad_step(R):
+    """36-layer 8B stack, batch 1, prefix 4096: one quadratic self-speculation step with chain length 7
+    (56 block rows, the benchmark's quadratic configuration) and the lambda = 0.5 ensemble verifier, its
+    speculative tokens from the oracle's own draft pass: logits of all rows and the decisions against the
+    rule on the GPU's own logits."""
+    from test_gpu_quad import check_step
+    wl, shape, _, B, plens, max_len, model, cache, okv, w = _setup(R, "8b", [0])
+    k, lam = 7, 0.5
+    anchor = synth_tokens(shape, wl.seed, "test.8b.quad.anchor", (1,))
+    log("8b quad: oracle draft pass for the speculative tokens")
+    spec, _ = O.draft_pass(w, okv, anchor, k)
+    spec = spec.astype(np.int32)
+    ws = R.QuadWorkspace(model, B, k, max_len)
+    res = R.quad_step(model, cache, ws, torch.from_numpy(anchor).cuda(), torch.from_numpy(spec).cuda(), k, lam,
+                      want_logits=True)
+    g = res["logits"].cpu().numpy()
+    log("8b quad: oracle quadratic pass")
+    ref, _, _ = O.quad_forward(w, okv, anchor, spec, k)
+    e = rel_err(g, ref)
+    log("8b quad k=%d lambda=%.1f: rel err %.3e, L=%d" % (k, lam, e, int(res["accept_len"].cpu()[0])))
+    assert e <= TOL
+    check_step(res, g, spec, k, lam, plens, cache)
+    assert R.read_device_status(ws) == 0
