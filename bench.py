@@ -140,6 +140,25 @@ def lora_timing(R, model, cache, ws, anchor, k, reps, wl):
     return res
 
 
+def traced_kernels(fn, n):
+    """Per kernel class: mean duration (us) of each launch and launches per call, over n eager calls of fn
+    with launch tracing on (HIP events recorded on each kernel's own dispatch)."""
+    import ctypes
+    import torch
+    from paper_2607_05722_amd import _lib as C
+    lib = C.load()
+    lib.nld_trace_enable(1)
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    ms = (ctypes.c_float * 8)()
+    cnt = (ctypes.c_int32 * 8)()
+    C.check(lib.nld_trace_read(ms, cnt, 8))
+    lib.nld_trace_enable(0)
+    return {name: {"avg_us": round(ms[i] / cnt[i] * 1e3, 2), "launches_per_call": cnt[i] // n}
+            for i, name in enumerate(C.TRACE_CLASSES) if cnt[i]}
+
+
 QUAD_K = 7   # chain length of the quadratic layout: k(k+1) = 56 block rows per sequence
 
 
@@ -171,6 +190,7 @@ def quad_timing(R, model, cache, anchor, reps):
 
     res = {"quad_ar": graph_ms(lambda: quad(1.0), reps), "quad_ensemble": graph_ms(lambda: quad(0.5), reps),
            "linear": graph_ms(linear, reps)}
+    res["kernels_us"] = traced_kernels(lambda: quad(0.5), 3)
     res["status"] = R.read_device_status(qws) | R.read_device_status(lws)
     cache.lengths.copy_(len0)
     torch.cuda.synchronize()
@@ -439,6 +459,7 @@ def main():
             "linear_step_ms_same_width": round(quad_ms["linear"], 4),
             "quad_hbm_frac": round(pass_bytes(shape, B, R_q, plens) / (quad_ms["quad_ar"] * 1e-3) / 1e9
                                    / HBM_PEAK_GBS, 4),
+            "kernels": quad_ms["kernels_us"],
         }
     if not args.no_cpu_baseline:
         del model, cache, ws

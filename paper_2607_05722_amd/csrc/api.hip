@@ -148,15 +148,17 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     L.keys = take(8 * L.Mpad * (size_t)L.lm_parts);
     L.lse = take(8 * L.Mpad * (size_t)L.lm_parts);   // softmax statistics per argmax partial (denoising)
     L.rope = take(8 * L.Mpad * (size_t)(c.head_dim / 2));
-    // split-K GEMM (M <= 32; the O, down and QKV projections): one counter per column group
-    // of at least 2 tiles, and the partials of up to SPLITK_MAX slices of 32-row groups
+    // split-K GEMM (M <= 64; the O, down, QKV and gate/up projections): one counter per column
+    // group of at least 2 tiles of the O, down and QKV projections, and the partials of up to
+    // SPLITK_MAX slices (gate/up, with more tiles, runs unsplit)
     const int sk_tiles = std::max((int)H / 16, (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim / 16);
-    L.n_sk_ctr = L.M <= 32 ? cdiv(sk_tiles, 2) : 0;
+    L.n_sk_ctr = L.M <= 64 ? cdiv(sk_tiles, 2) : 0;
+    const int sk_rows = L.M <= 32 ? 32 : 64;
     L.sk_ctr0 = 2 * c.n_layers + 1;
     // per pass: QKV and gate/up of every layer, LM head; then the split-K counters
     L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr));
-    // partials: whole column groups (at most 2 * n_sk_ctr + 4 tiles of 16) x 32 rows x slices
-    L.sk_part = take(L.M <= 32 ? 4 * (size_t)(2 * L.n_sk_ctr + 4) * 16 * 32 * SPLITK_MAX : 0);
+    // partials: whole column groups (at most 2 * n_sk_ctr + 4 tiles of 16) x sk_rows rows x slices
+    L.sk_part = take(L.M <= 64 ? 4 * (size_t)(2 * L.n_sk_ctr + 4) * 16 * sk_rows * SPLITK_MAX : 0);
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
     L.pml = take(4 * 2 * (size_t)L.units * L.n_parts * L.rows_pad);
     L.blk_k = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);   // block K/V, split: [unit][hi, lo][64][D]
@@ -227,10 +229,13 @@ int device_cus() {
 // Workgroups of the normed GEMM: one per CU, but at least two tiles per workgroup on
 // average (each workgroup loads the whole operand once); tiles beyond the first one per
 // workgroup are handed out dynamically.
-int norm_grid(int n_tiles) {
+// NLD_NORM_TPW_QKV / _GU / _LM: tiles per workgroup to aim for instead of 2.
+int norm_grid(int epi, int n_tiles) {
     const int cus = device_cus();
-    const int half = (n_tiles + 1) / 2;
-    return half < cus ? half : cus;
+    const int tpw = std::max(1, env_int(epi == EPI_QKV ? "NLD_NORM_TPW_QKV" : epi == EPI_SWIGLU ? "NLD_NORM_TPW_GU"
+                                                                                                : "NLD_NORM_TPW_LM", 2));
+    const int want = (n_tiles + tpw - 1) / tpw;
+    return want < cus ? want : cus;
 }
 
 struct StreamPlan {
@@ -309,20 +314,21 @@ bool use_tile(const GemmArgs& g) {
     return !env_int("NLD_NO_TILE_GEMM", 0) && !g.W2 && gemm_tile_supported(g.M, g.K, g.ksteps);
 }
 
-// Split-K plan of a projection with at most 32 rows: ct column tiles per workgroup and
-// ksplit K slices, so that column groups x slices is about one workgroup per CU, with
+// Split-K plan of a projection with at most 64 rows: ct column tiles per workgroup and
+// ksplit K slices, so that column groups x slices is at most one workgroup per CU, with
 // every wavefront (8 per workgroup) getting at least two k-steps.  Defaults per
-// projection (measured on MI355X at the 8B shapes): O 4 tiles; down 2 tiles; QKV off
-// (the normed multi-tile kernel is faster there).  Environment overrides:
-// NLD_SPLITK_<O|DOWN|QKV> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
+// projection (measured on MI355X at the 8B shapes): up to 16 rows O 4 tiles, down 2 tiles,
+// QKV and gate/up off (the normed multi-tile kernel is faster there); 17..64 rows every
+// projection 4 tiles.  Environment overrides:
+// NLD_SPLITK_<O|DOWN|QKV|GU> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
 // NLD_SPLITK / NLD_SPLITK_CT for every projection at once, NLD_NO_SPLITK = 1: off.
-enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2 };
+enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2, SK_GU = 3 };
 
 bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct, int* ksplit) {
     if (g.W2 || L.n_sk_ctr == 0 || env_int("NLD_NO_SPLITK", 0)) return false;
-    static const char* names[] = {"NLD_SPLITK_O", "NLD_SPLITK_DOWN", "NLD_SPLITK_QKV"};
-    static const int dflt_ct[] = {4, 2, 0};
-    int c = dflt_ct[kind], ks = 0;
+    static const char* names[] = {"NLD_SPLITK_O", "NLD_SPLITK_DOWN", "NLD_SPLITK_QKV", "NLD_SPLITK_GU"};
+    static const int dflt_ct[2][4] = {{4, 2, 0, 0}, {4, 4, 4, 4}};   // up to 16 rows; 17..64 rows
+    int c = dflt_ct[g.M > 16][kind], ks = 0;
     const char* v = getenv(names[kind]);
     if (v && *v) {
         c = atoi(v);
@@ -333,8 +339,8 @@ bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct,
     ks = env_int("NLD_SPLITK", ks);
     if (c <= 0 || !gemm_splitk_supported(epi, g.M, c)) return false;
     const int groups = cdiv(g.n_tiles, c);
-    if (groups > L.n_sk_ctr) return false;
-    if (ks <= 0) ks = std::min(std::max(1, (device_cus() + groups / 2) / groups), std::max(1, g.ksteps / 16));
+    if (ks <= 0) ks = std::min(std::max(1, device_cus() / groups), std::max(1, g.ksteps / 16));
+    if (groups > L.n_sk_ctr) ks = 1;   // no counters (and no partials) for that many groups
     *ct = c;
     *ksplit = std::max(1, std::min(std::min(ks, SPLITK_MAX), g.ksteps));
     return true;
@@ -360,11 +366,12 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     g.part_ss = at<float>(ws, L.part_ss);
     g.n_ss = g.K / 16;
     int ks = 0, waves = 0, ct = 0, ksplit = 0;
-    if (epi == EPI_QKV && plan_splitk(SK_QKV, epi, g, L, &ct, &ksplit))
+    if ((epi == EPI_QKV || (epi == EPI_SWIGLU && g.M > 16)) &&
+        plan_splitk(epi == EPI_QKV ? SK_QKV : SK_GU, epi, g, L, &ct, &ksplit))
         return launch_gemm_splitk(epi, ct, ksplit, g, at<float>(ws, L.sk_part),
                                   at<unsigned>(ws, L.tile_ctr) + L.sk_ctr0, s);
     if (plan_norm(epi, g.M, g.ksteps, &ks, &waves)) {
-        const int grid = norm_grid(g.n_tiles);
+        const int grid = norm_grid(epi, g.n_tiles);
         if (parts_out) *parts_out = grid;
         g.n_parts = grid;
         return launch_gemm_norm(epi, ks, waves, grid, g, s);

@@ -609,8 +609,8 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
 }
 
 // =====================================================================================
-// Split-K GEMM (O and down projections with the residual epilogue, and the normed QKV
-// projection; M <= 32).  Workgroup (column group cg,
+// Split-K GEMM (O and down projections with the residual epilogue, and the normed QKV and
+// gate/up projections; M <= 64).  Workgroup (column group cg,
 // K slice ks) multiplies its slice of the operand against CT column tiles, so the
 // operand is read once per CT tiles and K slice instead of once per tile (the split
 // operand is twice as large as the weights it multiplies in these projections).  The
@@ -624,13 +624,24 @@ hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int g
 // the next launch and runs the residual epilogue.  No workgroup ever waits for
 // another: there is no spin and no cache-wide fence.
 // =====================================================================================
+// Operand and weight registers of one batch of the split-K GEMM: U k-steps.
+template <int MT, int CT, int U>
+struct SkBatch {
+    uint4 w[U][CT];
+    uint4 x[U][MT];
+    uint4 xl[U][MT];
+};
+
 template <int MT, int CT, int NW, int EPI>
 __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float* part, unsigned* ctr, int ksplit) {
-    typedef Batch<MT, CT, true> B;
-    constexpr int U = B::U;
-    constexpr int NTL = MT * CT;   // output tiles of the workgroup; wavefront w < NTL finishes tile w
+    // Up to two row tiles: separate hi and lo accumulators and batches of several k-steps.  Four row
+    // tiles: one accumulator per output tile takes both operand halves and a batch is one k-step
+    // (the registers of 16 tiles' accumulators and of 12 operand quads per k-step).
+    constexpr bool MERGE = MT >= 4;
+    constexpr int U = MERGE ? 1 : Batch<MT, CT, true>::U;
+    typedef SkBatch<MT, CT, U> B;
+    constexpr int NTL = MT * CT;   // output tiles of the workgroup; wavefront w finishes tiles w, w + NW, ...
     constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU;
-    static_assert(NTL <= NW, "one wavefront per output tile in the epilogue");
     static_assert(EPI == EPI_RESID || NORMED, "residual, QKV or SwiGLU epilogue");
     __shared__ f32x4_t red[NW][NTL][64];
     __shared__ float inv_s[16 * MT];
@@ -649,16 +660,18 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
     const int s_begin = min(ke, kb + wave * per);
     const int s_end = min(ke, s_begin + per);
 
-    // epilogue inputs of this wavefront's tile, fetched up front: residual rows 4g + i
+    // epilogue inputs of this wavefront's first tile, fetched up front: residual rows 4g + i
     // of the tile and the next RMSNorm gain of column r
-    const int my_mt = wave / CT, my_t = t0 + wave % CT;
     float xres[4] = {0.f, 0.f, 0.f, 0.f}, gn = 0.f;
-    if (EPI == EPI_RESID && wave < NTL && my_t < a.n_tiles) {
-        gn = bf16_to_f32(a.gain_next[my_t * 16 + r]);
+    if (EPI == EPI_RESID && wave < NTL) {
+        const int mt = wave / CT, t = t0 + wave % CT;
+        if (t < a.n_tiles) {
+            gn = bf16_to_f32(a.gain_next[t * 16 + r]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int m = 16 * my_mt + 4 * g + i;
-            if (m < a.M) xres[i] = a.x[(size_t)m * N + my_t * 16 + r];
+            for (int i = 0; i < 4; ++i) {
+                const int m = 16 * mt + 4 * g + i;
+                if (m < a.M) xres[i] = a.x[(size_t)m * N + t * 16 + r];
+            }
         }
     }
 
@@ -673,11 +686,17 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
         ap[mt] = a.A + (size_t)mt * a.ksteps * 1024 + (size_t)lane * 8;
     }
 
-    f32x4_t acc[MT][CT], accl[MT][CT];
+    f32x4_t acc[MT][CT], accl[MERGE ? 1 : MT][MERGE ? 1 : CT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = accl[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int ct = 0; ct < CT; ++ct) acc[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if constexpr (!MERGE) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) accl[mt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
 
     const uint4 zero4 = {0u, 0u, 0u, 0u};
     auto load = [&](int s, B& buf) __attribute__((always_inline)) {
@@ -704,7 +723,8 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct) {
                     acc[mt][ct] = mfma_16x16x32(buf.x[u][mt], buf.w[u][ct], acc[mt][ct]);
-                    accl[mt][ct] = mfma_16x16x32(buf.xl[u][mt], buf.w[u][ct], accl[mt][ct]);
+                    if constexpr (MERGE) acc[mt][ct] = mfma_16x16x32(buf.xl[u][mt], buf.w[u][ct], acc[mt][ct]);
+                    else accl[mt][ct] = mfma_16x16x32(buf.xl[u][mt], buf.w[u][ct], accl[mt][ct]);
                 }
     };
 
@@ -720,21 +740,37 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) red[wave][mt * CT + ct][lane] = acc[mt][ct] + accl[mt][ct];
+        for (int ct = 0; ct < CT; ++ct) {
+            if constexpr (MERGE) red[wave][mt * CT + ct][lane] = acc[mt][ct];
+            else red[wave][mt * CT + ct][lane] = acc[mt][ct] + accl[mt][ct];
+        }
     __syncthreads();
 
-    // the workgroup's partial of tile `wave` (fixed order over the wavefronts)
-    f32x4_t v = {0.f, 0.f, 0.f, 0.f};
-    if (wave < NTL) {
+    typedef unsigned long long u64;
+    // the workgroup's partials of the wavefront's tiles ti = wave, wave + NW, ... (fixed order over
+    // the wavefronts), kept in registers and, with ksplit > 1, stored for the last workgroup
+    constexpr int TPW = (NTL + NW - 1) / NW;
+    f32x4_t v[TPW];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) v += red[w][wave][lane];
+    for (int q = 0; q < TPW; ++q) {
+        const int ti = wave + q * NW;
+        v[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        if (ti < NTL) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) v[q] += red[w][ti][lane];
+        }
     }
     if (ksplit > 1) {
-        typedef unsigned long long u64;
-        u64* pp = (u64*)(part + ((((size_t)cg * ksplit + ks) * NTL + wave) * 64 + lane) * 4);
-        if (wave < NTL) {
-            __hip_atomic_store(pp, __builtin_bit_cast(u64, f32x2_t{v[0], v[1]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(pp + 1, __builtin_bit_cast(u64, f32x2_t{v[2], v[3]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int q = 0; q < TPW; ++q) {
+            const int ti = wave + q * NW;
+            if (ti < NTL) {
+                u64* pp = (u64*)(part + ((((size_t)cg * ksplit + ks) * NTL + ti) * 64 + lane) * 4);
+                __hip_atomic_store(pp, __builtin_bit_cast(u64, f32x2_t{v[q][0], v[q][1]}), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(pp + 1, __builtin_bit_cast(u64, f32x2_t{v[q][2], v[q][3]}), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
         // every lane's stores are acknowledged before the workgroup counts itself in
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -746,64 +782,82 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
         __syncthreads();
         if (!last_s) return;
         if (threadIdx.x == 0) __hip_atomic_exchange(ctr + cg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (wave < NTL) {
+#pragma unroll
+        for (int q = 0; q < TPW; ++q) {
+            const int ti = wave + q * NW;
+            if (ti >= NTL) continue;
             f32x4_t sum = {0.f, 0.f, 0.f, 0.f};
             for (int sl = 0; sl < ksplit; ++sl) {
                 if (sl == ks) {
-                    sum += v;
+                    sum += v[q];
                     continue;
                 }
-                const u64* q = (const u64*)(part + ((((size_t)cg * ksplit + sl) * NTL + wave) * 64 + lane) * 4);
-                const f32x2_t lo = __builtin_bit_cast(f32x2_t, __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                const f32x2_t hi = __builtin_bit_cast(f32x2_t, __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const u64* qq = (const u64*)(part + ((((size_t)cg * ksplit + sl) * NTL + ti) * 64 + lane) * 4);
+                const f32x2_t lo = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const f32x2_t hi = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qq + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
                 sum += f32x4_t{lo[0], lo[1], hi[0], hi[1]};
             }
-            v = sum;
+            v[q] = sum;
         }
     }
-    if (wave >= NTL || my_t >= a.n_tiles) return;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = 16 * my_mt + 4 * g + i;
-        if constexpr (EPI == EPI_RESID) {
-            epi_resid(a, v[i], m, my_t, lane, xres[i], gn);
-        } else if constexpr (EPI == EPI_QKV) {
-            const int mc = min(m, a.M - 1);
-            const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
-            epi_qkv(a, v[i] * inv_s[m], m, my_t, lane, pos);
-        } else {
-            epi_swiglu(a, v[i] * inv_s[m], m, my_t, lane);
+    for (int q = 0; q < TPW; ++q) {
+        const int ti = wave + q * NW;
+        if (ti >= NTL) continue;
+        const int mt = ti / CT, t = t0 + ti % CT;
+        if (t >= a.n_tiles) continue;
+        if (EPI == EPI_RESID && q > 0) {
+            gn = bf16_to_f32(a.gain_next[t * 16 + r]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = 16 * mt + 4 * g + i;
+                xres[i] = m < a.M ? a.x[(size_t)m * N + t * 16 + r] : 0.f;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = 16 * mt + 4 * g + i;
+            if constexpr (EPI == EPI_RESID) {
+                epi_resid(a, v[q][i], m, t, lane, xres[i], gn);
+            } else if constexpr (EPI == EPI_QKV) {
+                const int mc = min(m, a.M - 1);
+                const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
+                epi_qkv(a, v[q][i] * inv_s[m], m, t, lane, pos);
+            } else {
+                epi_swiglu(a, v[q][i] * inv_s[m], m, t, lane);
+            }
         }
     }
 }
 
 bool gemm_splitk_supported(int epi, int M, int ct) {
-    return (epi == EPI_RESID || epi == EPI_QKV || epi == EPI_SWIGLU) && M >= 1 && M <= 32 && ct >= 2 && ct <= 4;
+    return (epi == EPI_RESID || epi == EPI_QKV || epi == EPI_SWIGLU) && M >= 1 && M <= 64 && ct >= 2 && ct <= 4;
 }
 
 template <int EPI, int CT>
-static void launch_splitk_ct(dim3 grid, bool two, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
+static void launch_splitk_ct(dim3 grid, int mt, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
                              hipStream_t s) {
-    if (two) launch(gemm_splitk_kernel<2, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
+    if (mt == 4) launch(gemm_splitk_kernel<4, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
+    else if (mt == 2) launch(gemm_splitk_kernel<2, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
     else launch(gemm_splitk_kernel<1, CT, 8, EPI>, grid, dim3(512), s, a, part, ctr, ksplit);
 }
 
 template <int EPI>
-static void launch_splitk_epi(int ct, dim3 grid, bool two, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
+static void launch_splitk_epi(int ct, dim3 grid, int mt, const GemmArgs& a, float* part, unsigned* ctr, int ksplit,
                               hipStream_t s) {
-    if (ct == 4) launch_splitk_ct<EPI, 4>(grid, two, a, part, ctr, ksplit, s);
-    else if (ct == 3) launch_splitk_ct<EPI, 3>(grid, two, a, part, ctr, ksplit, s);
-    else launch_splitk_ct<EPI, 2>(grid, two, a, part, ctr, ksplit, s);
+    if (ct == 4) launch_splitk_ct<EPI, 4>(grid, mt, a, part, ctr, ksplit, s);
+    else if (ct == 3) launch_splitk_ct<EPI, 3>(grid, mt, a, part, ctr, ksplit, s);
+    else launch_splitk_ct<EPI, 2>(grid, mt, a, part, ctr, ksplit, s);
 }
 
 hipError_t launch_gemm_splitk(int epi, int ct, int ksplit, const GemmArgs& a, float* part, unsigned* ctr,
                               hipStream_t s) {
     if (!gemm_splitk_supported(epi, a.M, ct) || a.W2 || ksplit < 1 || ksplit > SPLITK_MAX) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((a.n_tiles + ct - 1) / ct), (unsigned)ksplit);
-    const bool two = a.M > 16;
-    if (epi == EPI_RESID) launch_splitk_epi<EPI_RESID>(ct, grid, two, a, part, ctr, ksplit, s);
-    else if (epi == EPI_QKV) launch_splitk_epi<EPI_QKV>(ct, grid, two, a, part, ctr, ksplit, s);
-    else launch_splitk_epi<EPI_SWIGLU>(ct, grid, two, a, part, ctr, ksplit, s);
+    const int mt = a.M > 32 ? 4 : (a.M > 16 ? 2 : 1);
+    if (epi == EPI_RESID) launch_splitk_epi<EPI_RESID>(ct, grid, mt, a, part, ctr, ksplit, s);
+    else if (epi == EPI_QKV) launch_splitk_epi<EPI_QKV>(ct, grid, mt, a, part, ctr, ksplit, s);
+    else launch_splitk_epi<EPI_SWIGLU>(ct, grid, mt, a, part, ctr, ksplit, s);
     return hipGetLastError();
 }
 

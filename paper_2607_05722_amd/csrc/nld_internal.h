@@ -254,9 +254,10 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // With a.W2 set (EPI_RESID only) the reduction continues over the second source.
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
-// Split-K GEMM (EPI_RESID, EPI_QKV or EPI_SWIGLU; M <= 32, no second source): ct column
+// Split-K GEMM (EPI_RESID, EPI_QKV or EPI_SWIGLU; M <= 64, no second source): ct column
 // tiles per workgroup (2..4), the reduction cut into ksplit slices (1..SPLITK_MAX) whose
-// partials meet in `part` (ceil(n_tiles/ct) * ksplit * 16*ct*ceil(M/16) floats); `ctr`
+// partials meet in `part` (ceil(n_tiles/ct) * ksplit * 256*ct*MT floats, MT = 1, 2 or 4 row
+// tiles for M <= 16, 32, 64; unused with ksplit = 1); `ctr`
 // holds one counter per column group, zero before the launch and zero again after it.
 // The normed epilogues take the per-row RMSNorm scale from part_ss as the other GEMMs do.
 constexpr int SPLITK_MAX = 8;

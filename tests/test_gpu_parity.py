@@ -444,3 +444,24 @@ def test_8b_layer_split_k_repeatable(R, layer8b, monkeypatch, k, qkv):
         again, _ = R.block_forward(t["model"], t["cache"], ws, tt, R.VERIFY)
         assert np.array_equal(again.cpu().numpy(), first), "pass %d differs" % (i + 1)
     assert R.read_device_status(ws) == 0
+
+
+@pytest.mark.parametrize("k,ksplit", [(24, 3), (40, 3), (64, 8)])
+def test_tiny_split_k_many_rows(R, tiny, monkeypatch, k, ksplit):
+    """17..64 rows: every projection (QKV, O, gate/up, down) on the split-K kernel with two or four row
+    tiles (four: one accumulator per tile for both operand halves), ksplit ragged K slices; verify and
+    draft passes against the oracle."""
+    t = tiny
+    monkeypatch.setenv("NLD_SPLITK", str(ksplit))
+    block = synth_tokens(t["shape"], 0, "tiny.block%d" % k, (1, k))
+    ws = R.Workspace(t["model"], 1, k, 256)
+    for mode in (O.VERIFY, O.DRAFT):
+        ref, _, _ = O.block_forward(t["w"], t["okv"], block, mode)
+        logits, am = R.block_forward(t["model"], t["cache"], ws, torch.from_numpy(block).cuda(),
+                                     R.VERIFY if mode == O.VERIFY else R.DRAFT)
+        g = logits.cpu().numpy()
+        e = rel_err(g, ref)
+        log("tiny split-K k=%d ksplit=%d %s: rel err %.3e" % (k, ksplit, mode, e))
+        assert e <= TOL
+        check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+    assert R.read_device_status(ws) == 0
