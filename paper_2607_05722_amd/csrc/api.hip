@@ -165,9 +165,10 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     L.blk_v = take(2 * (size_t)L.units * 2 * 64 * c.head_dim);
     L.lora_t = take(4 * (size_t)L.Mpad * c.lora_rank);   // split lora_scale * (A o), draft passes only
     L.drafts = take(4 * (size_t)batch * k);              // nld_decode_steps: one step's drafts
-    // quadratic self-speculation: the verifier rows' logits [batch][2 quad_k][vocab] and tokens [batch][quad_k]
+    // quadratic self-speculation: the verifier rows' logits [batch][2 quad_k][vocab] and the ensemble's
+    // argmax keys [batch][quad_k][ENS_CHUNKS]
     L.ens_logits = take(4 * (size_t)batch * 2 * quad_k * c.vocab);
-    L.ens_v = take(4 * (size_t)batch * quad_k);
+    L.ens_v = take(8 * (size_t)batch * quad_k * ENS_CHUNKS);
     L.total = off;
     return L;
 }
@@ -618,7 +619,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         fa.quad_k = io.quad_k;
         fa.lambda = io.lambda;
         fa.ens_logits = at<float>(ws, L.ens_logits);
-        fa.ens_v = at<int32_t>(ws, L.ens_v);
+        fa.ens_keys = at<unsigned long long>(ws, L.ens_v);
+        fa.ens_chunks = ENS_CHUNKS;
         TraceScope ts(NLD_TRACE_ARGMAX, s);
         if (ensemble) HIP_TRY(launch_quad_ensemble(fa, s));
         HIP_TRY(launch_quad_finish(fa, s));

@@ -1671,12 +1671,15 @@ __device__ __forceinline__ float2 row_lse(const FinishArgs& a, int m, int lane) 
     return st;
 }
 
-// One workgroup per (sequence b, position i): v_{i+1} = argmax over the vocabulary of
-// lambda * exp(a_n - A) / SA + (1 - lambda) * exp(d_n - D) / SD (lowest index on ties).
-__global__ void __launch_bounds__(1024) quad_ensemble_kernel(FinishArgs a) {
+// Workgroup (sequence b and position i, vocabulary chunk ch): the argmax key over the chunk
+// of lambda * exp(a_n - A) / SA + (1 - lambda) * exp(d_n - D) / SD (lowest index on ties),
+// into ens_keys[(b * quad_k + i) * ens_chunks + ch].  Each thread has eight columns of both
+// rows in flight at a time.
+__global__ void __launch_bounds__(512) quad_ensemble_kernel(FinishArgs a) {
     __shared__ float2 st_s[2];
-    __shared__ unsigned long long key_s[16];
-    const int b = blockIdx.x, i = blockIdx.y, qk = a.quad_k, R = a.k_blk, V = a.vocab;
+    __shared__ unsigned long long key_s[8];
+    const int qk = a.quad_k, R = a.k_blk, V = a.vocab;
+    const int bi = blockIdx.x, b = bi / qk, i = bi % qk, ch = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     if (wave < 2) {
         const float2 st = row_lse(a, b * R + (wave == 0 ? i : qk + i * qk), lane);
@@ -1687,10 +1690,23 @@ __global__ void __launch_bounds__(1024) quad_ensemble_kernel(FinishArgs a) {
     const float ca = a.lambda / sa.y, cd = (1.0f - a.lambda) / sd.y;
     const float* la = a.ens_logits + ((size_t)b * 2 * qk + i) * V;
     const float* ld = a.ens_logits + ((size_t)b * 2 * qk + qk + i) * V;
+    const int per = (V + a.ens_chunks - 1) / a.ens_chunks;
+    const int n0 = ch * per, n1 = min(V, n0 + per), nt = blockDim.x;
     unsigned long long best = 0ull;
-    for (int n = threadIdx.x; n < V; n += blockDim.x) {
-        const float p = ca * expf(la[n] - sa.x) + cd * expf(ld[n] - sd.x);
-        best = umax64(best, argmax_key(p, (uint32_t)n));
+    for (int n = n0 + (int)threadIdx.x; n < n1; n += 8 * nt) {
+        float xa[8], xd[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = n + u * nt;
+            xa[u] = j < n1 ? la[j] : 0.f;
+            xd[u] = j < n1 ? ld[j] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = n + u * nt;
+            const float p = ca * expf(xa[u] - sa.x) + cd * expf(xd[u] - sd.x);
+            if (j < n1) best = umax64(best, argmax_key(p, (uint32_t)j));
+        }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) best = umax64(best, __shfl_xor(best, off));
@@ -1699,7 +1715,7 @@ __global__ void __launch_bounds__(1024) quad_ensemble_kernel(FinishArgs a) {
     if (threadIdx.x == 0) {
         unsigned long long k2 = 0ull;
         for (int w = 0; w < nw; ++w) k2 = umax64(k2, key_s[w]);
-        a.ens_v[b * qk + i] = argmax_key_index(k2);
+        a.ens_keys[(size_t)bi * a.ens_chunks + ch] = k2;
     }
 }
 
@@ -1712,8 +1728,15 @@ __global__ void __launch_bounds__(1024) quad_finish_kernel(FinishArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     for (int i = wave; i < qk; i += nw) {
         int32_t v;
-        if (a.lambda > 0.0f && a.lambda < 1.0f) v = a.ens_v[b * qk + i];
-        else v = row_argmax(a, b * R + (a.lambda >= 1.0f ? i : qk + i * qk), lane);
+        if (a.lambda > 0.0f && a.lambda < 1.0f) {   // the ensemble kernel's per-chunk keys
+            unsigned long long best = 0ull;
+            for (int c = lane; c < a.ens_chunks; c += 64) best = umax64(best, a.ens_keys[(size_t)(b * qk + i) * a.ens_chunks + c]);
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) best = umax64(best, __shfl_xor(best, off));
+            v = argmax_key_index(best);
+        } else {
+            v = row_argmax(a, b * R + (a.lambda >= 1.0f ? i : qk + i * qk), lane);
+        }
         if (lane == 0) v_s[i] = v;
     }
     __syncthreads();
@@ -1736,7 +1759,7 @@ __global__ void __launch_bounds__(1024) quad_finish_kernel(FinishArgs a) {
 }
 
 hipError_t launch_quad_ensemble(const FinishArgs& a, hipStream_t s) {
-    launch(quad_ensemble_kernel, dim3(a.batch, a.quad_k), dim3(1024), s, a);
+    launch(quad_ensemble_kernel, dim3(a.batch * a.quad_k, a.ens_chunks), dim3(512), s, a);
     return hipGetLastError();
 }
 

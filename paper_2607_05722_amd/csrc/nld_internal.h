@@ -217,11 +217,13 @@ struct FinishArgs {
     // FINISH_QUAD: chain length quad_k (k_blk = quad_k * (quad_k + 1) rows per sequence); draft_in
     // holds the speculative tokens [batch][quad_k - 1], draft_out receives the next ones; the
     // verifier is the AR row (lambda >= 1), the diffusion row (lambda <= 0) or, in between, the
-    // ensemble kernel's tokens in ens_v [batch][quad_k] (from ens_logits and part_lse).
+    // ensemble kernel's argmax keys ens_keys [batch][quad_k][ens_chunks] (one per vocabulary
+    // chunk, from ens_logits and part_lse).
     int quad_k;
     float lambda;
     const float* ens_logits;
-    int32_t* ens_v;
+    unsigned long long* ens_keys;
+    int ens_chunks;
 };
 
 enum PackKind { PACK_LINEAR = 0, PACK_QKV = 1, PACK_GATE_UP = 2 };
@@ -276,8 +278,9 @@ hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& a, hipStream_t s);
-// Quadratic self-speculation: the ensemble verifier's tokens (0 < lambda < 1; grid batch x quad_k),
-// then acceptance, commit and the next speculative tokens (grid batch).
+// Quadratic self-speculation: the ensemble verifier's per-chunk keys (0 < lambda < 1; grid
+// batch*quad_k x ens_chunks), then acceptance, commit and the next speculative tokens (grid batch).
+constexpr int ENS_CHUNKS = 32;
 hipError_t launch_quad_ensemble(const FinishArgs& a, hipStream_t s);
 hipError_t launch_quad_finish(const FinishArgs& a, hipStream_t s);
 
