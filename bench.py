@@ -269,6 +269,29 @@ def measured_traffic(kernel):
         return None
 
 
+def copy_ceiling(gib=2, reps=5):
+    """Practical HBM ceiling: GB/s (bytes read + written) of a plain device-to-device copy of `gib` GiB,
+    alternating between two buffer pairs so that no copy finds its source in the memory-side cache."""
+    import torch
+    n = gib * (1 << 30) // 4
+    bufs = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(4)]
+    for b in bufs:
+        b.fill_(1.0)
+    bufs[1].copy_(bufs[0])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        src, dst = (bufs[0], bufs[1]) if i % 2 == 0 else (bufs[2], bufs[3])
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = 2.0 * n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del bufs
+    torch.cuda.empty_cache()
+    return round(gbps, 1)
+
+
 def copy_calibration(mib, reps=3):
     """Plain device-to-device copies of a known size, for scaling the counters of a --pmc run."""
     import torch
@@ -450,6 +473,8 @@ def main():
                                           * (shape.q_dim + shape.hidden)) / (lora_ms["lora_draft"] * 1e-3) / 1e9
                                          / HBM_PEAK_GBS, 4),
         }
+    if not args.no_extras:
+        res["hbm_copy_GBps"] = copy_ceiling()   # what a plain copy reaches on this part (read + write)
     if quad_ms is not None:
         R_q = QUAD_K * (QUAD_K + 1)
         res["quad_ss"] = {
