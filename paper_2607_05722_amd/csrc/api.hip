@@ -318,9 +318,9 @@ bool use_tile(const GemmArgs& g) {
 // Split-K plan of a projection with at most 64 rows: ct column tiles per workgroup and
 // ksplit K slices, so that column groups x slices is at most one workgroup per CU, with
 // every wavefront (8 per workgroup) getting at least two k-steps.  Defaults per
-// projection (measured on MI355X at the 8B shapes): up to 16 rows O 4 tiles, down 2 tiles,
-// QKV and gate/up off (the normed multi-tile kernel is faster there); 17..64 rows every
-// projection 4 tiles.  Environment overrides:
+// projection (measured on MI355X at the 8B shapes): up to 16 rows down 2 tiles, O off (the
+// streamed GEMM, 11.3 against 12.9 us), QKV and gate/up off (the normed multi-tile kernel is
+// faster there); 17..64 rows every projection 4 tiles.  Environment overrides:
 // NLD_SPLITK_<O|DOWN|QKV|GU> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
 // NLD_SPLITK / NLD_SPLITK_CT for every projection at once, NLD_NO_SPLITK = 1: off.
 enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2, SK_GU = 3 };
@@ -328,7 +328,7 @@ enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2, SK_GU = 3 };
 bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct, int* ksplit) {
     if (g.W2 || L.n_sk_ctr == 0 || env_int("NLD_NO_SPLITK", 0)) return false;
     static const char* names[] = {"NLD_SPLITK_O", "NLD_SPLITK_DOWN", "NLD_SPLITK_QKV", "NLD_SPLITK_GU"};
-    static const int dflt_ct[2][4] = {{4, 2, 0, 0}, {4, 4, 4, 4}};   // up to 16 rows; 17..64 rows
+    static const int dflt_ct[2][4] = {{0, 2, 0, 0}, {4, 4, 4, 4}};   // up to 16 rows; 17..64 rows
     int c = dflt_ct[g.M > 16][kind], ks = 0;
     const char* v = getenv(names[kind]);
     if (v && *v) {
