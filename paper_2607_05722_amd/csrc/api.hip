@@ -96,8 +96,10 @@ namespace {
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
     int n_sk_ctr, sk_ctr0;   // split-K residual GEMM: counters (one per column group) from tile counter sk_ctr0
+    int n_nk_ctr, nk_ctr0;   // normed GEMM of 17..64 rows: counters (one per column tile) from tile counter nk_ctr0
+    size_t nk_part_floats;   // and the size of its partials buffer
     size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, sk_part, lora_t, drafts,
-        ens_logits, ens_v, total;
+        ens_logits, ens_v, nk_part, total;
 };
 
 // k: block rows per sequence.  quad_k > 0: the block is a quadratic self-speculation layout
@@ -155,8 +157,20 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     L.n_sk_ctr = L.M <= 64 ? cdiv(sk_tiles, 2) : 0;
     const int sk_rows = L.M <= 32 ? 32 : 64;
     L.sk_ctr0 = 2 * c.n_layers + 1;
-    // per pass: QKV and gate/up of every layer, LM head; then the split-K counters
-    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr));
+    // normed GEMM of 17..64 rows: one counter per column tile of the widest normed projection,
+    // partials of every K slice
+    const int nk_tiles = std::max(std::max(cdiv(c.vocab, 16), cdiv(c.ffn, 8)),
+                                  (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim / 16);
+    const bool nk = L.M > 16 && L.M <= 64;
+    L.n_nk_ctr = nk ? nk_tiles : 0;
+    L.nk_ctr0 = L.sk_ctr0 + L.n_sk_ctr;
+    // per pass: QKV and gate/up of every layer, LM head; then the split-K counters and the
+    // 17..64-row counters (all zeroed by the embedding kernel at the start of a pass)
+    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr));
+    L.nk_part_floats = nk ? (size_t)nk_tiles * cdiv(cdiv((int)H, 32), gemm_normk_kstep_span(L.M)) *
+                                (L.M > 32 ? 4 : 2) * 256
+                          : 0;
+    L.nk_part = take(4 * L.nk_part_floats);
     // partials: whole column groups (at most 2 * n_sk_ctr + 4 tiles of 16) x sk_rows rows x slices
     L.sk_part = take(L.M <= 64 ? 4 * (size_t)(2 * L.n_sk_ctr + 4) * 16 * sk_rows * SPLITK_MAX : 0);
     L.po = take(4 * (size_t)L.units * L.n_parts * L.rows_pad * c.head_dim);
@@ -367,6 +381,19 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     g.part_ss = at<float>(ws, L.part_ss);
     g.n_ss = g.K / 16;
     int ks = 0, waves = 0, ct = 0, ksplit = 0;
+    const int nk_slices = cdiv(g.ksteps, gemm_normk_kstep_span(g.M));
+    if (L.n_nk_ctr > 0 && gemm_normk_supported(epi, g.M) && !env_int("NLD_NO_NORMK", 0) &&
+        g.n_tiles <= L.n_nk_ctr && cdiv(g.n_tiles, gemm_normk_max_tiles()) * nk_slices <= L.lm_parts &&
+        (size_t)g.n_tiles * nk_slices * (g.M > 32 ? 4 : 2) * 256 <= L.nk_part_floats) {
+        // 17..64 rows: K slices of the operand held in registers, about one workgroup per CU
+        const int slices = nk_slices;
+        int gx = std::max(cdiv(g.n_tiles, gemm_normk_max_tiles()), std::max(1, device_cus() / slices));
+        // the LM head writes one argmax key per row and workgroup: at most lm_parts per row
+        if (epi == EPI_LMHEAD) gx = std::min(gx, std::max(1, L.lm_parts / slices));
+        g.n_parts = gx * slices;
+        if (parts_out) *parts_out = g.n_parts;
+        return launch_gemm_normk(epi, gx, g, at<float>(ws, L.nk_part), at<unsigned>(ws, L.tile_ctr) + L.nk_ctr0, s);
+    }
     if ((epi == EPI_QKV || (epi == EPI_SWIGLU && g.M > 16)) &&
         plan_splitk(epi == EPI_QKV ? SK_QKV : SK_GU, epi, g, L, &ct, &ksplit))
         return launch_gemm_splitk(epi, ct, ksplit, g, at<float>(ws, L.sk_part),
@@ -415,7 +442,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.status = status;
     e.rope = at<float2>(ws, L.rope);
     e.tile_ctr = at<unsigned>(ws, L.tile_ctr);
-    e.n_tile_ctr = 2 * c.n_layers + 1 + L.n_sk_ctr;
+    e.n_tile_ctr = 2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr;
     e.lengths = kv->lengths;
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;

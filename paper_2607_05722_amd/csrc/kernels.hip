@@ -349,6 +349,255 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 }
 
 // =====================================================================================
+// Normed multi-tile GEMM for 17..64 rows (QKV, gate/up, LM head of a pass with two or four
+// row tiles, such as the quadratic self-speculation pass).  The operand of MT row tiles is
+// too large to reload per column tile (the split operand is 2 KB per row tile and k-step,
+// against 1 KB of weights per column tile), so a workgroup of 8 wavefronts holds one K
+// slice of it in registers for every column tile it multiplies: wavefront w owns k-steps
+// [(ks*8 + w)*KS, +KS) of slice ks = blockIdx.y.  Workgroup x of a slice takes column tiles
+// x, x + gridDim.x, ...; their weights stream through PF register buffers, each refilled
+// with the tile PF ahead as soon as it has been multiplied.  Per tile the wavefronts'
+// products meet in LDS and the slice's partial goes to the workspace with agent-scope
+// stores.  After its last tile the workgroup counts itself in on each tile's counter; the
+// workgroup that completes a tile reads the slices' partials in slice order and runs the
+// epilogue (wavefront w takes row tile w % MT of every (8/MT)-th completed tile), then
+// resets the counter.
+// =====================================================================================
+constexpr int NK_MAXT = 160;   // column tiles per workgroup (the host keeps ceil(n_tiles / grid.x) within it)
+
+template <int MT, int KS, int PF, int EPI>
+__global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part, unsigned* tctr, int ksplit) {
+    constexpr int NW = 8;
+    constexpr int WPR = NW / MT;   // wavefronts per row tile in the epilogue
+    static_assert(NW % MT == 0, "row tiles must divide the wavefronts");
+    __shared__ f32x4_t red[2][NW][MT][64];
+    __shared__ float inv_s[16 * MT];
+    __shared__ unsigned char last_s[NK_MAXT];
+    __shared__ int fin_s[NK_MAXT];
+    __shared__ int nfin_s;
+    __shared__ unsigned long long key_s[NW][16];
+    __shared__ float2 lse_s[NW][16];
+    typedef unsigned long long u64;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int x = blockIdx.x, Gx = gridDim.x, ks = blockIdx.y;
+    const int T = a.n_tiles;
+    const int nt = x < T ? (T - 1 - x) / Gx + 1 : 0;
+    const int s0 = (ks * NW + wave) * KS;
+    const uint4 zero4 = {0u, 0u, 0u, 0u};
+
+    // this wavefront's operand slice, hi and lo, for every row tile
+    uint4 ah[MT][KS], al[MT][KS];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            const int ss = s0 + s;
+            const bool ok = mt * 16 + r < a.M && ss < a.ksteps && ss * 32 + 8 * g < a.K;
+            const uint16_t* ap = a.A + (size_t)(mt * a.ksteps + ss) * 1024 + (size_t)lane * 8;
+            ah[mt][s] = zero4;
+            al[mt][s] = zero4;
+            if (ok) {
+                ah[mt][s] = *(const uint4*)ap;
+                al[mt][s] = *(const uint4*)(ap + SPLIT_LO);
+            }
+        }
+
+    rms_scales(a, 0, 16 * MT, inv_s);   // visible after the first barrier below
+    if constexpr (EPI == EPI_LMHEAD) {
+        if (threadIdx.x < NW * 16) {
+            key_s[threadIdx.x / 16][threadIdx.x % 16] = 0ull;
+            lse_s[threadIdx.x / 16][threadIdx.x % 16] = float2{-INFINITY, 0.f};
+        }
+    }
+    if (nt == 0) return;   // no column tile here (the whole workgroup leaves; the LM head writes no key)
+
+    // Per tile, every wavefront stores EL elements of one row tile's partial: row tile w % MT,
+    // elements (w / MT) * EL .. +EL of each lane's four (one 8-byte store, or one 4-byte store).
+    constexpr int EL = 4 / WPR;
+    static_assert(EL == 1 || EL == 2, "one 4- or 8-byte partial store per wavefront and tile");
+    const int st_mt = wave % MT, st_e0 = (wave / MT) * EL;
+    auto store_part = [&](int t, f32x4_t v) __attribute__((always_inline)) {
+        float* pp = part + ((((size_t)t * ksplit + ks) * MT + st_mt) * 64 + lane) * 4 + st_e0;
+        if constexpr (EL == 2)
+            __hip_atomic_store((u64*)pp, __builtin_bit_cast(u64, f32x2_t{v[st_e0], v[st_e0 + 1]}), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        else
+            __hip_atomic_store(pp, v[st_e0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+
+    // Weight loads are unconditional, with the tile and the k-step clamped into the matrix (a
+    // k-step past the end meets a zero operand; a tile past the workgroup's last is never
+    // multiplied).  Each buffer's loads are followed by one partial store, here a zero into the
+    // first tile's slot that its real partial overwrites later, so that the prologue leaves the
+    // same sequence of outstanding loads and stores as a loop iteration: the wait counts then
+    // stay exact and the next PF tiles' loads remain in flight across the loop.
+    const int s_last = a.ksteps - 1;
+    uint4 wb[PF][KS];
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            wb[p][s] = a.W[((size_t)min(x + p * Gx, T - 1) * a.ksteps + min(s0 + s, s_last)) * 64 + lane];
+        store_part(x, f32x4_t{0.f, 0.f, 0.f, 0.f});
+    }
+
+    // epilogue of row tile mt of tile t from its full sum v (lane layout of an MFMA result);
+    // LM head: the row maxima and statistics accumulate per wavefront in LDS (rows 4g + i)
+    auto epilogue = [&](f32x4_t v, int t, int mt) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = 16 * mt + 4 * g + i;
+            const float y = v[i] * inv_s[m];
+            if constexpr (EPI == EPI_QKV) {
+                const int mc = min(m, a.M - 1);
+                const int pos = committed_length(a.lengths, mc / a.k_blk, a.max_len, a.status) + mc % a.k_blk;
+                epi_qkv(a, y, m, t, lane, pos);
+            } else if constexpr (EPI == EPI_SWIGLU) {
+                epi_swiglu(a, y, m, t, lane);
+            } else {
+                float2 tl;
+                const u64 key = epi_lmhead(a, y, m, t, lane, &tl);
+                if (r == 0) {
+                    key_s[wave][4 * g + i] = umax64(key_s[wave][4 * g + i], key);
+                    if (a.part_lse) lse_s[wave][4 * g + i] = lse_merge(lse_s[wave][4 * g + i], tl);
+                }
+            }
+        }
+    };
+
+    // tile j (the workgroup's j-th) from buffer p, whose next tile is j + PF
+    auto tile = [&](int j, int p_dummy, uint4 (&w)[KS]) __attribute__((always_inline)) {
+        (void)p_dummy;
+        const int t = x + j * Gx;
+        f32x4_t acc[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const int tn = min(x + (j + PF) * Gx, T - 1);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                acc[mt] = mfma_16x16x32(ah[mt][s], w[s], acc[mt]);
+                acc[mt] = mfma_16x16x32(al[mt][s], w[s], acc[mt]);
+            }
+            w[s] = a.W[((size_t)tn * a.ksteps + min(s0 + s, s_last)) * 64 + lane];
+        }
+        const int par = j & 1;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) red[par][wave][mt][lane] = acc[mt];
+        __syncthreads();
+        // the slice's partial: this wavefront's elements of row tile st_mt (fixed order over
+        // the wavefronts)
+        f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int w2 = 0; w2 < NW; ++w2) v += red[par][w2][st_mt][lane];
+        store_part(t, v);
+    };
+    // whole groups of PF tiles with no condition inside, so the loop keeps one shape; then the rest
+    int j0 = 0;
+    for (; j0 + PF <= nt; j0 += PF) {
+#pragma unroll
+        for (int p = 0; p < PF; ++p) tile(j0 + p, p, wb[p]);
+    }
+#pragma unroll
+    for (int p = 0; p < PF - 1; ++p)
+        if (j0 + p < nt) tile(j0 + p, p, wb[p]);
+
+    {   // the tiles this workgroup completes (with a single slice: all of its own)
+        // every lane's partial stores are acknowledged before the workgroup counts itself in
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __syncthreads();
+        for (int j = threadIdx.x; j < nt; j += blockDim.x)
+            last_s[j] = __hip_atomic_fetch_add(tctr + x + j * Gx, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                        (unsigned)(ksplit - 1);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int n = 0;
+            for (int j = 0; j < nt; ++j)
+                if (last_s[j]) fin_s[n++] = x + j * Gx;
+            nfin_s = n;
+        }
+        __syncthreads();
+        const int nfin = nfin_s;
+        for (int c = threadIdx.x; c < nfin; c += blockDim.x)
+            __hip_atomic_exchange(tctr + fin_s[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // wavefront w: row tile w % MT of completed tiles w / MT, + WPR, ...; two tiles' partials in flight
+        const int mt = wave % MT;
+        for (int c = wave / MT; c < nfin; c += 2 * WPR) {
+            const int c2 = c + WPR;
+            const int ta = fin_s[c], tb = c2 < nfin ? fin_s[c2] : ta;
+            f32x4_t va = {0.f, 0.f, 0.f, 0.f}, vb = {0.f, 0.f, 0.f, 0.f};
+            for (int sl = 0; sl < ksplit; ++sl) {
+                const u64* qa = (const u64*)(part + ((((size_t)ta * ksplit + sl) * MT + mt) * 64 + lane) * 4);
+                const u64* qb = (const u64*)(part + ((((size_t)tb * ksplit + sl) * MT + mt) * 64 + lane) * 4);
+                const f32x2_t a0 = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qa, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const f32x2_t a1 = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qa + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const f32x2_t b0 = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                const f32x2_t b1 = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qb + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                va += f32x4_t{a0[0], a0[1], a1[0], a1[1]};
+                vb += f32x4_t{b0[0], b0[1], b1[0], b1[1]};
+            }
+            epilogue(va, ta, mt);
+            if (c2 < nfin) epilogue(vb, tb, mt);
+        }
+    }
+
+    if constexpr (EPI == EPI_LMHEAD) {
+        // one argmax key (and softmax statistics) per row for this workgroup
+        __syncthreads();
+        if ((int)threadIdx.x < 16 * MT) {
+            const int m = threadIdx.x, mt = m / 16, rl = m % 16;
+            if (m < a.M) {
+                u64 k2 = 0ull;
+                float2 st = float2{-INFINITY, 0.f};
+                for (int w = mt; w < NW; w += MT) {   // the wavefronts that finished row tile mt
+                    k2 = umax64(k2, key_s[w][rl]);
+                    st = lse_merge(st, lse_s[w][rl]);
+                }
+                const int part_id = x + Gx * ks;
+                a.part_keys[(size_t)m * a.n_parts + part_id] = k2;
+                if (a.part_lse) a.part_lse[(size_t)m * a.n_parts + part_id] = st;
+            }
+        }
+    }
+}
+
+bool gemm_normk_supported(int epi, int M) {
+    return (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_LMHEAD) && M > 16 && M <= 64;
+}
+
+int gemm_normk_kstep_span(int) { return 8 * 4; }   // k-steps per slice: 8 wavefronts x 4
+
+int gemm_normk_max_tiles() { return NK_MAXT; }
+
+template <int MT, int KS>
+static hipError_t launch_normk_mt(int epi, dim3 grid, const GemmArgs& a, float* part, unsigned* tctr, int ksplit,
+                                  hipStream_t s) {
+    constexpr int PF = MT >= 4 ? 3 : 4;   // tiles of weights in flight per wavefront (registers permitting)
+    switch (epi) {
+        case EPI_QKV: launch(gemm_normk_kernel<MT, KS, PF, EPI_QKV>, grid, dim3(512), s, a, part, tctr, ksplit); break;
+        case EPI_SWIGLU: launch(gemm_normk_kernel<MT, KS, PF, EPI_SWIGLU>, grid, dim3(512), s, a, part, tctr, ksplit); break;
+        case EPI_LMHEAD: launch(gemm_normk_kernel<MT, KS, PF, EPI_LMHEAD>, grid, dim3(512), s, a, part, tctr, ksplit); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_normk(int epi, int grid_x, const GemmArgs& a, float* part, unsigned* tctr, hipStream_t s) {
+    if (!gemm_normk_supported(epi, a.M) || grid_x < 1) return hipErrorInvalidValue;
+    if ((a.n_tiles + grid_x - 1) / grid_x > NK_MAXT) return hipErrorInvalidValue;
+    const int span = gemm_normk_kstep_span(a.M);
+    const int ksplit = (a.ksteps + span - 1) / span;
+    const dim3 grid((unsigned)grid_x, (unsigned)ksplit);
+    if (a.M > 32) return launch_normk_mt<4, 4>(epi, grid, a, part, tctr, ksplit, s);
+    return launch_normk_mt<2, 4>(epi, grid, a, part, tctr, ksplit, s);
+}
+
+// =====================================================================================
 // Streamed GEMM: out[m][n] = sum_k A[m][k] W[n][k] for 16*MT rows x 16*CT columns per
 // workgroup; the NW wavefronts split the reduction, each streaming its slice of the
 // weights and of the bf16 activations with one batch in flight ahead of the MFMAs.

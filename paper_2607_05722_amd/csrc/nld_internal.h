@@ -256,6 +256,15 @@ hipError_t launch_gemm_norm(int epi, int ks, int waves, int grid, const GemmArgs
 // With a.W2 set (EPI_RESID only) the reduction continues over the second source.
 hipError_t launch_gemm_stream(int epi, int mt, int ct, int nw, int grid_x, int grid_y, const GemmArgs& a,
                               hipStream_t s);
+// Normed multi-tile GEMM for 17..64 rows (EPI_QKV, EPI_SWIGLU, EPI_LMHEAD) with the K split
+// into slices of gemm_normk_kstep_span(M) k-steps (grid grid_x x slices); the slices meet in
+// `part` (n_tiles * slices * 256 * MT floats) through one counter per column tile in `tctr`
+// (zero before the launch and zero again after it).  LM head: n_parts = grid_x * slices.
+// Needs ceil(n_tiles / grid_x) <= gemm_normk_max_tiles().
+bool gemm_normk_supported(int epi, int M);
+int gemm_normk_kstep_span(int M);
+int gemm_normk_max_tiles();
+hipError_t launch_gemm_normk(int epi, int grid_x, const GemmArgs& a, float* part, unsigned* tctr, hipStream_t s);
 // Split-K GEMM (EPI_RESID, EPI_QKV or EPI_SWIGLU; M <= 64, no second source): ct column
 // tiles per workgroup (2..4), the reduction cut into ksplit slices (1..SPLITK_MAX) whose
 // partials meet in `part` (ceil(n_tiles/ct) * ksplit * 256*ct*MT floats, MT = 1, 2 or 4 row

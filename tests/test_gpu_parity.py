@@ -50,7 +50,7 @@ INT_SHAPE = ModelShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_d
                        rms_eps=0.0)
 
 
-@pytest.mark.parametrize("k", [1, 8, 40, 64])
+@pytest.mark.parametrize("k", [1, 8, 12, 28, 40, 64])
 def test_lm_head_integer_exact(R, k):
     """Embedding gather, LM-head packing/tiling (ragged vocab 1000) and the fused argmax: the logits are
     exact integers on both sides, so they must agree bit for bit, ties included (lowest index wins)."""
@@ -70,11 +70,12 @@ def test_lm_head_integer_exact(R, k):
     assert R.read_device_status(ws) == 0
 
 
-@pytest.mark.parametrize("prefix", [0, 5, 61])
-def test_qkv_value_rows_integer_exact(R, prefix):
+@pytest.mark.parametrize("prefix,k", [(0, 8), (5, 8), (61, 8), (5, 24), (61, 56)])
+def test_qkv_value_rows_integer_exact(R, prefix, k):
     """QKV packing, the V cache's transposed 64-position tiles and the cache row addressing: with +-1
-    activations and {-1,0,1} Wv the block's V rows are exact integers; K rows are zero."""
-    shape, seed, k = INT_SHAPE, 22, 8
+    activations and {-1,0,1} Wv the block's V rows are exact integers; K rows are zero.  24 and 56
+    rows run the QKV projection on the 17..64-row kernel (K slices met through the workspace)."""
+    shape, seed = INT_SHAPE, 22
     src = _int_model(shape, seed, wv_int=True)
     tok = synth_tokens(shape, seed, "int.tokens", (1, k))
     w = O.OracleWeights(shape, src, np.float64)
