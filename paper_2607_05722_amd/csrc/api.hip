@@ -167,6 +167,7 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     // per pass: QKV and gate/up of every layer, LM head; then the split-K counters and the
     // 17..64-row counters (all zeroed by the embedding kernel at the start of a pass)
     L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr));
+    // (the normed projections, LM head, QKV and gate/up, all reduce over hidden)
     L.nk_part_floats = nk ? (size_t)nk_tiles * cdiv(cdiv((int)H, 32), gemm_normk_kstep_span(L.M)) *
                                 (L.M > 32 ? 4 : 2) * 256
                           : 0;
@@ -361,8 +362,28 @@ bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct,
     return true;
 }
 
-// Residual projections (O, down): the tiled GEMM when it applies, the split-K GEMM for
-// up to 32 rows, else the streamed one.
+// The multi-tile GEMM of 17..64 rows when it applies (counters and partials fit the
+// workspace); returns false otherwise.
+bool try_normk(int epi, GemmArgs& g, void* ws, const Layout& L, hipStream_t s, int* parts_out, hipError_t* err) {
+    if (L.n_nk_ctr == 0 || !gemm_normk_supported(epi, g.M) || g.W2 || env_int("NLD_NO_NORMK", 0)) return false;
+    const int slices = cdiv(g.ksteps, gemm_normk_kstep_span(g.M));
+    if (g.n_tiles > L.n_nk_ctr || cdiv(g.n_tiles, gemm_normk_max_tiles()) * slices > L.lm_parts ||
+        (size_t)g.n_tiles * slices * (g.M > 32 ? 4 : 2) * 256 > L.nk_part_floats)
+        return false;
+    // about one workgroup per CU; the LM head writes one argmax key per row and workgroup (at most
+    // lm_parts per row)
+    int gx = std::max(cdiv(g.n_tiles, gemm_normk_max_tiles()), std::max(1, device_cus() / slices));
+    if (epi == EPI_LMHEAD) gx = std::min(gx, std::max(1, L.lm_parts / slices));
+    g.n_parts = gx * slices;
+    if (parts_out) *parts_out = g.n_parts;
+    *err = launch_gemm_normk(epi, gx, g, at<float>(ws, L.nk_part), at<unsigned>(ws, L.tile_ctr) + L.nk_ctr0, s);
+    return true;
+}
+
+// Residual projections (O, down): the tiled GEMM when it applies, the split-K GEMM for up to
+// 64 rows, else the streamed one.  (The multi-tile GEMM of 17..64 rows with the residual
+// epilogue was slower at 56 rows: down 60.5 against 35.1 us, its 12 K slices' partials
+// dominating.)
 hipError_t resid_gemm(int kind, const GemmArgs& g, void* ws, const Layout& L, hipStream_t s) {
     if (use_tile(g)) return launch_gemm_tile(EPI_RESID, g, s);
     int ct = 0, ksplit = 0;
@@ -381,19 +402,8 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     g.part_ss = at<float>(ws, L.part_ss);
     g.n_ss = g.K / 16;
     int ks = 0, waves = 0, ct = 0, ksplit = 0;
-    const int nk_slices = cdiv(g.ksteps, gemm_normk_kstep_span(g.M));
-    if (L.n_nk_ctr > 0 && gemm_normk_supported(epi, g.M) && !env_int("NLD_NO_NORMK", 0) &&
-        g.n_tiles <= L.n_nk_ctr && cdiv(g.n_tiles, gemm_normk_max_tiles()) * nk_slices <= L.lm_parts &&
-        (size_t)g.n_tiles * nk_slices * (g.M > 32 ? 4 : 2) * 256 <= L.nk_part_floats) {
-        // 17..64 rows: K slices of the operand held in registers, about one workgroup per CU
-        const int slices = nk_slices;
-        int gx = std::max(cdiv(g.n_tiles, gemm_normk_max_tiles()), std::max(1, device_cus() / slices));
-        // the LM head writes one argmax key per row and workgroup: at most lm_parts per row
-        if (epi == EPI_LMHEAD) gx = std::min(gx, std::max(1, L.lm_parts / slices));
-        g.n_parts = gx * slices;
-        if (parts_out) *parts_out = g.n_parts;
-        return launch_gemm_normk(epi, gx, g, at<float>(ws, L.nk_part), at<unsigned>(ws, L.tile_ctr) + L.nk_ctr0, s);
-    }
+    hipError_t err = hipSuccess;
+    if (try_normk(epi, g, ws, L, s, parts_out, &err)) return err;   // 17..64 rows
     if ((epi == EPI_QKV || (epi == EPI_SWIGLU && g.M > 16)) &&
         plan_splitk(epi == EPI_QKV ? SK_QKV : SK_GU, epi, g, L, &ct, &ksplit))
         return launch_gemm_splitk(epi, ct, ksplit, g, at<float>(ws, L.sk_part),

@@ -447,13 +447,16 @@ def test_8b_layer_split_k_repeatable(R, layer8b, monkeypatch, k, qkv):
     assert R.read_device_status(ws) == 0
 
 
-@pytest.mark.parametrize("k,ksplit", [(24, 3), (40, 3), (64, 8)])
+@pytest.mark.parametrize("k,ksplit", [(24, 3), (40, 3), (64, 8), (24, 0), (56, 0)])
 def test_tiny_split_k_many_rows(R, tiny, monkeypatch, k, ksplit):
-    """17..64 rows: every projection (QKV, O, gate/up, down) on the split-K kernel with two or four row
-    tiles (four: one accumulator per tile for both operand halves), ksplit ragged K slices; verify and
-    draft passes against the oracle."""
+    """17..64 rows.  ksplit > 0: every projection (QKV, O, gate/up, down) on the split-K kernel with two
+    or four row tiles (four: one accumulator per tile for both operand halves), ksplit ragged K slices.
+    ksplit = 0: the default plan, the multi-tile kernel that holds the operand's K slice in registers
+    (the LM head too).  Verify and draft passes against the oracle."""
     t = tiny
-    monkeypatch.setenv("NLD_SPLITK", str(ksplit))
+    if ksplit:
+        monkeypatch.setenv("NLD_NO_NORMK", "1")
+        monkeypatch.setenv("NLD_SPLITK", str(ksplit))
     block = synth_tokens(t["shape"], 0, "tiny.block%d" % k, (1, k))
     ws = R.Workspace(t["model"], 1, k, 256)
     for mode in (O.VERIFY, O.DRAFT):
