@@ -64,6 +64,19 @@ def pass_bytes(shape, batch, k, prefix_lens):
         + kb["lm_head"]
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16
+
+
+def pass_flops(shape, batch, k, prefix_lens):
+    """Algorithmic flops of one pass: 2 per weight element and block row, plus 4 * head_dim per query head,
+    block row and visible key (every block row counted against the whole prefix + block)."""
+    M, H, F, V = batch * k, shape.hidden, shape.ffn, shape.vocab
+    QD, KVD, L = shape.q_dim, shape.kv_dim, shape.n_layers
+    w_elems = L * (H * (QD + 2 * KVD) + QD * H + 2 * H * F + F * H) + V * H
+    keys = int(np.sum(np.asarray(prefix_lens) + k)) * k
+    return 2 * M * w_elems + 4 * shape.n_q_heads * shape.head_dim * L * keys
+
+
 def refresh_bytes(shape, batch, k, prefix_lens):
     """A refresh runs every layer's QKV but stops after the last one: no attention, FFN or LM head after it."""
     kb = kernel_bytes(shape, batch, k, prefix_lens)
@@ -447,6 +460,10 @@ def main():
         "step_hbm_GBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
         "step_hbm_frac": round(bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_step": int(bytes_step),
+        "mfma": {"algorithmic_TFLOPs": round(2 * pass_flops(shape, B, k, plens) / (ms_per_step * 1e-3) / 1e12, 2),
+                 "frac_of_bf16_peak": round(2 * pass_flops(shape, B, k, plens) / (ms_per_step * 1e-3) / 1e12
+                                            / MFMA_BF16_PEAK_TFLOPS, 4),
+                 "note": "split activation operands run two MFMAs per product: the issued MFMA work is about twice this"},
         "committed_tokens_per_s": round(committed / (elapsed_ms * 1e-3), 1),
         "device_status": status,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
