@@ -305,6 +305,51 @@ def copy_ceiling(gib=2, reps=5):
     return round(gbps, 1)
 
 
+def read_ceiling(gib=4, reps=5):
+    """GB/s of a device-wide sum over `gib` GiB (reads only; torch's reduction kernel)."""
+    import torch
+    n = gib * (1 << 30) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    x.sum()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        x.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x
+    torch.cuda.empty_cache()
+    return round(gbps, 1)
+
+
+def layer_microbench(R, reps=20):
+    """One 8B-shaped layer + LM head (batch 1, prefix 2048, seeded weights and K/V): mean ms of a verify
+    pass and of a draft pass at k = 8, 16 and 32, each replayed from a captured graph."""
+    import torch
+    from synth.workloads import LazyWeights, WORKLOADS, prefix_kv, tokens
+    wl = WORKLOADS["8b_layer"]
+    shape, P = wl.shape, wl.prefix_len
+    model = R.DeviceModel(shape, LazyWeights(shape, wl.seed, keep=False))
+    cache = R.DeviceCache(shape, 1, P + 64)
+    kb, vb = prefix_kv(shape, wl.seed, 0, 1, P)
+    cache.load_prefix(0, kb, vb)
+    cache.set_lengths([P])
+    out = {}
+    for k in wl.k_values:
+        ws = R.Workspace(model, 1, k, P + 64)
+        tok = torch.from_numpy(tokens(shape, wl.seed, "bench.layer.block%d" % k, (1, k))).cuda()
+        res = {}
+        for name, mode in (("verify", R.VERIFY), ("draft", R.DRAFT)):
+            ms = graph_ms(lambda: R.block_forward(model, cache, ws, tok, mode, want_logits=False), reps)
+            res[name + "_pass_ms"] = round(ms, 4)
+            res[name + "_hbm_frac"] = round(pass_bytes(shape, 1, k, [P]) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        out["k=%d" % k] = res
+    model.close()
+    return out
+
+
 def copy_calibration(mib, reps=3):
     """Plain device-to-device copies of a known size, for scaling the counters of a --pmc run."""
     import torch
@@ -415,12 +460,13 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
-        m2_ms = lora_ms = quad_ms = None
+        m2_ms = lora_ms = quad_ms = layer_ms = None
         if not args.no_extras:
             block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
             m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
             lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
             quad_ms = quad_timing(R, model, cache, anchor, max(5, steps // 2))
+            layer_ms = layer_microbench(R)
             status |= R.read_device_status(ws) | lora_ms["status"] | quad_ms["status"]
 
     ms_per_step = elapsed_ms / steps
@@ -492,6 +538,8 @@ def main():
         }
     if not args.no_extras:
         res["hbm_copy_GBps"] = copy_ceiling()   # what a plain copy reaches on this part (read + write)
+        res["hbm_sum_read_GBps"] = read_ceiling()   # and a plain reduction (reads only)
+        res["layer_microbench"] = layer_ms
     if quad_ms is not None:
         R_q = QUAD_K * (QUAD_K + 1)
         res["quad_ss"] = {
