@@ -570,14 +570,15 @@ bool gemm_normk_supported(int epi, int M) {
     return (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_LMHEAD) && M > 16 && M <= 64;
 }
 
-int gemm_normk_kstep_span(int) { return 8 * 4; }   // k-steps per slice: 8 wavefronts x 4
+// k-steps per slice: 8 wavefronts x 4 (four row tiles) or x 8 (two row tiles)
+int gemm_normk_kstep_span(int M) { return 8 * (M > 32 ? 4 : 8); }
 
 int gemm_normk_max_tiles() { return NK_MAXT; }
 
 template <int MT, int KS>
 static hipError_t launch_normk_mt(int epi, dim3 grid, const GemmArgs& a, float* part, unsigned* tctr, int ksplit,
                                   hipStream_t s) {
-    constexpr int PF = MT >= 4 ? 3 : 4;   // tiles of weights in flight per wavefront (registers permitting)
+    constexpr int PF = MT >= 4 ? 3 : 2;   // tiles of weights in flight per wavefront (registers permitting)
     switch (epi) {
         case EPI_QKV: launch(gemm_normk_kernel<MT, KS, PF, EPI_QKV>, grid, dim3(512), s, a, part, tctr, ksplit); break;
         case EPI_SWIGLU: launch(gemm_normk_kernel<MT, KS, PF, EPI_SWIGLU>, grid, dim3(512), s, a, part, tctr, ksplit); break;
@@ -594,7 +595,7 @@ hipError_t launch_gemm_normk(int epi, int grid_x, const GemmArgs& a, float* part
     const int ksplit = (a.ksteps + span - 1) / span;
     const dim3 grid((unsigned)grid_x, (unsigned)ksplit);
     if (a.M > 32) return launch_normk_mt<4, 4>(epi, grid, a, part, tctr, ksplit, s);
-    return launch_normk_mt<2, 4>(epi, grid, a, part, tctr, ksplit, s);
+    return launch_normk_mt<2, 8>(epi, grid, a, part, tctr, ksplit, s);
 }
 
 // =====================================================================================
