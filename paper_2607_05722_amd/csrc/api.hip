@@ -97,8 +97,10 @@ struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
     int n_sk_ctr, sk_ctr0;   // split-K residual GEMM: counters (one per column group) from tile counter sk_ctr0
     int n_nk_ctr, nk_ctr0;   // normed GEMM of 17..64 rows: counters (one per column tile) from tile counter nk_ctr0
+    int n_tk_ctr, tk_ctr0;   // tiled GEMM with K slices (M > 64): counters (one per tile group) from tk_ctr0
+    int tk_part_wgs;         // (tile group, slice) partials its buffer holds
     size_t nk_part_floats;   // and the size of its partials buffer
-    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, sk_part, lora_t, drafts,
+    size_t status, x, xg, part_ss, q, o, act, keys, lse, rope, po, pml, blk_k, blk_v, tile_ctr, sk_part, tk_part, lora_t, drafts,
         ens_logits, ens_v, nk_part, total;
 };
 
@@ -166,7 +168,17 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     L.nk_ctr0 = L.sk_ctr0 + L.n_sk_ctr;
     // per pass: QKV and gate/up of every layer, LM head; then the split-K counters and the
     // 17..64-row counters (all zeroed by the embedding kernel at the start of a pass)
-    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr));
+    // tiled GEMM (M > 64) with K slices: one counter per 128 x 128 tile group of the widest
+    // projection it may split (O, down, QKV, gate/up), partials of up to two workgroups per CU
+    const bool tk = L.M > 64;
+    L.n_tk_ctr = tk ? std::max(gemm_tile_groups(L.M, std::max(sk_tiles, cdiv(c.ffn, 8))), 1) : 0;
+    L.tk_ctr0 = L.nk_ctr0 + L.n_nk_ctr;
+    L.tk_part_wgs = tk ? 2 * gemm_tile_wgs_per_cu() * device_cus() : 0;
+    // per pass: QKV and gate/up of every layer, LM head; then the split-K counters, the 17..64-row
+    // counters and the tiled GEMM's counters (all zeroed by the embedding kernel at the start of a
+    // pass; the split GEMMs also reset theirs after each use)
+    L.tile_ctr = take(4 * (size_t)(2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr + L.n_tk_ctr));
+    L.tk_part = take(4 * (size_t)L.tk_part_wgs * gemm_tile_part_floats_per_wg());
     // (the normed projections, LM head, QKV and gate/up, all reduce over hidden)
     L.nk_part_floats = nk ? (size_t)nk_tiles * cdiv(cdiv((int)H, 32), gemm_normk_kstep_span(L.M)) *
                                 (L.M > 32 ? 4 : 2) * 256
@@ -330,6 +342,29 @@ bool use_tile(const GemmArgs& g) {
     return !env_int("NLD_NO_TILE_GEMM", 0) && !g.W2 && gemm_tile_supported(g.M, g.K, g.ksteps);
 }
 
+enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2, SK_GU = 3 };
+
+// K slices of the tiled GEMM (M > 64): enough slices to fill every CU's workgroup slots when the
+// 128 x 128 tile groups alone leave CUs idle (O, down and QKV at a few hundred rows; gate/up has
+// several groups per CU already), each slice at least two stages of 64 k.
+// NLD_TILE_KSPLIT_<O|DOWN|QKV|GU> overrides the count (1: off).
+int plan_tile_ksplit(int kind, const GemmArgs& g, const Layout& L) {
+    static const char* names[] = {"NLD_TILE_KSPLIT_O", "NLD_TILE_KSPLIT_DOWN", "NLD_TILE_KSPLIT_QKV",
+                                  "NLD_TILE_KSPLIT_GU"};
+    const int groups = gemm_tile_groups(g.M, g.n_tiles);
+    int ks = kind == SK_GU ? 1 : std::max(1, gemm_tile_wgs_per_cu() * device_cus() / groups);
+    ks = env_int(names[kind], ks);
+    ks = std::min(ks, std::min(gemm_tile_stages(g.ksteps) / 2, 8));
+    if (ks <= 1 || groups > L.n_tk_ctr || groups * ks > L.tk_part_wgs) return 1;
+    return ks;
+}
+
+hipError_t tile_gemm(int kind, int epi, const GemmArgs& g, void* ws, const Layout& L, hipStream_t s) {
+    const int ks = epi == EPI_LMHEAD ? 1 : plan_tile_ksplit(kind, g, L);
+    if (ks == 1) return launch_gemm_tile(epi, g, 1, nullptr, nullptr, s);
+    return launch_gemm_tile(epi, g, ks, at<float>(ws, L.tk_part), at<unsigned>(ws, L.tile_ctr) + L.tk_ctr0, s);
+}
+
 // Split-K plan of a projection with at most 64 rows: ct column tiles per workgroup and
 // ksplit K slices, so that column groups x slices is at most one workgroup per CU, with
 // every wavefront (8 per workgroup) getting at least two k-steps.  Defaults per
@@ -338,7 +373,6 @@ bool use_tile(const GemmArgs& g) {
 // faster there); 17..64 rows every projection 4 tiles.  Environment overrides:
 // NLD_SPLITK_<O|DOWN|QKV|GU> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
 // NLD_SPLITK / NLD_SPLITK_CT for every projection at once, NLD_NO_SPLITK = 1: off.
-enum SplitKind { SK_O = 0, SK_DOWN = 1, SK_QKV = 2, SK_GU = 3 };
 
 bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct, int* ksplit) {
     if (g.W2 || L.n_sk_ctr == 0 || env_int("NLD_NO_SPLITK", 0)) return false;
@@ -385,7 +419,7 @@ bool try_normk(int epi, GemmArgs& g, void* ws, const Layout& L, hipStream_t s, i
 // epilogue was slower at 56 rows: down 60.5 against 35.1 us, its 12 K slices' partials
 // dominating.)
 hipError_t resid_gemm(int kind, const GemmArgs& g, void* ws, const Layout& L, hipStream_t s) {
-    if (use_tile(g)) return launch_gemm_tile(EPI_RESID, g, s);
+    if (use_tile(g)) return tile_gemm(kind, EPI_RESID, g, ws, L, s);
     int ct = 0, ksplit = 0;
     if (plan_splitk(kind, EPI_RESID, g, L, &ct, &ksplit))
         return launch_gemm_splitk(EPI_RESID, ct, ksplit, g, at<float>(ws, L.sk_part),
@@ -417,7 +451,7 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     if (use_tile(g)) {
         g.n_parts = gemm_tile_parts(g.n_tiles);
         if (parts_out) *parts_out = g.n_parts;
-        return launch_gemm_tile(epi, g, s);
+        return tile_gemm(epi == EPI_QKV ? SK_QKV : SK_GU, epi, g, ws, L, s);
     }
     const StreamPlan p = plan_stream(epi, g.M, g.n_tiles);
     if (parts_out) *parts_out = p.gx;
@@ -452,7 +486,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.status = status;
     e.rope = at<float2>(ws, L.rope);
     e.tile_ctr = at<unsigned>(ws, L.tile_ctr);
-    e.n_tile_ctr = 2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr;
+    e.n_tile_ctr = 2 * c.n_layers + 1 + L.n_sk_ctr + L.n_nk_ctr + L.n_tk_ctr;
     e.lengths = kv->lengths;
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;

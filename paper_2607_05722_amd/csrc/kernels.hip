@@ -1126,17 +1126,24 @@ hipError_t launch_gemm_splitk(int epi, int ct, int ksplit, const GemmArgs& a, fl
 namespace tile {
 constexpr int BR = 8;                        // row tiles per workgroup
 constexpr int BC = 8;                        // column tiles per workgroup
-constexpr int KS = 2;                        // k-steps per stage
+constexpr int KS = 1;                        // k-steps per stage
 constexpr int A_CHUNKS = BR * KS * 2;        // 1 KiB operand blocks per stage (hi and lo)
 constexpr int W_CHUNKS = BC * KS;            // 1 KiB weight blocks per stage
 constexpr int CHUNKS = A_CHUNKS + W_CHUNKS;
 constexpr int NT = 512;
 constexpr int CPT = CHUNKS * 64 / NT;        // 16-byte pieces per thread per stage
+constexpr int PD = 4;                        // stages in flight in registers (even: LDS buffer = stage & 1)
+static_assert(PD % 2 == 0, "the LDS buffer of a stage is its parity");
 static_assert(A_CHUNKS * 64 % NT == 0 && CHUNKS * 64 % NT == 0, "pieces per thread must split by kind");
 }  // namespace tile
 
+// K slices: with ksplit > 1, workgroup (x, y) multiplies the y-th of ksplit near-equal runs of
+// stages of its 128 x 128 tile and stores its accumulators to `part` with agent-scope stores; the
+// workgroup that completes the tile's counter adds the slices in slice order and runs the
+// epilogue, then resets the counter.
 template <int EPI>
-__global__ void __launch_bounds__(512) gemm_tile_kernel(GemmArgs a, int R, int C) {
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
+gemm_tile_kernel(GemmArgs a, int R, int C, int ksplit, float* part, unsigned* ctr) {
     using namespace tile;
     constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LMHEAD;
     __shared__ uint4 lds[2][CHUNKS * 64];
@@ -1175,8 +1182,12 @@ __global__ void __launch_bounds__(512) gemm_tile_kernel(GemmArgs a, int R, int C
     // 128; column tiles past the end are read clamped and their outputs dropped.  So every
     // load is unconditional and in bounds.
     static_assert(A_CHUNKS % 8 == 0 && CHUNKS == 8 * CPT, "8 blocks per piece index");
-    const int nst = a.ksteps / KS;
-    const uint4* srcp[CPT];   // stage 0 address of each piece
+    // slice ksl: stages [ksl*n/ksplit, (ksl+1)*n/ksplit), at least one since ksplit <= n
+    const int ksl = blockIdx.y;
+    const int nst_all = a.ksteps / KS;
+    const int st0 = ksl * nst_all / ksplit;
+    const int nst = (ksl + 1) * nst_all / ksplit - st0;
+    const uint4* srcp[CPT];   // stage 0 address of each piece (the slice's first stage)
 #pragma unroll
     for (int q = 0; q < CPT; ++q) {
         const int chunk = wave + 8 * q;
@@ -1187,6 +1198,7 @@ __global__ void __launch_bounds__(512) gemm_tile_kernel(GemmArgs a, int R, int C
             const int wck = chunk - A_CHUNKS, ct = wck / KS, ks = wck % KS;
             srcp[q] = a.W + ((size_t)min(c * BC + ct, a.n_tiles - 1) * a.ksteps + ks) * 64 + lane;
         }
+        srcp[q] += (size_t)st0 * KS * (q < A_CHUNKS / 8 ? 128 : 64);
     }
     // stage st: operand blocks advance by KS k-steps of 2 KiB, weight blocks by KS of 1 KiB
     typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -1226,27 +1238,88 @@ __global__ void __launch_bounds__(512) gemm_tile_kernel(GemmArgs a, int R, int C
         }
     };
 
-    // Stage s is multiplied from LDS buffer s & 1 while stage s+1 waits in registers and
-    // stage s+2 is in flight (unrolled by two so that no register copy waits on a load still
-    // in flight; loads past the last stage re-read it and are never stored).
-    u32x4_t r0[CPT], r1[CPT];
-    NLD_TILE_GLOAD(0, r0);
-    NLD_TILE_GLOAD(min(1, nst - 1), r1);
-    NLD_TILE_LSTORE(r0, 0);
+    // Stage s is multiplied from LDS buffer s & 1 while stages s+1 .. s+PD wait or are in flight in
+    // a ring of PD register slots: the slot of stage s is refilled with stage s+PD as soon as s is
+    // in LDS, so PD stages of loads cover the L2 / HBM latency.  The loop is unrolled by PD so
+    // that every slot index is a compile-time constant; loads past the last stage re-read it and
+    // are never stored.
+    u32x4_t rb[PD][CPT];
+#pragma unroll
+    for (int p = 0; p < PD; ++p) NLD_TILE_GLOAD(min(p, nst - 1), rb[p]);
+    NLD_TILE_LSTORE(rb[0], 0);
     __syncthreads();
-    for (int st = 0; st < nst; st += 2) {
-        NLD_TILE_GLOAD(min(st + 2, nst - 1), r0);
-        compute(0);
-        if (st + 1 < nst) { NLD_TILE_LSTORE(r1, 1); }
-        __syncthreads();
-        if (st + 1 >= nst) break;
-        NLD_TILE_GLOAD(min(st + 3, nst - 1), r1);
-        compute(1);
-        if (st + 2 < nst) { NLD_TILE_LSTORE(r0, 0); }
-        __syncthreads();
+    for (int st = 0; st < nst; st += PD) {
+#pragma unroll
+        for (int u = 0; u < PD; ++u) {
+            const int cur = st + u;
+            if (cur >= nst) break;
+            NLD_TILE_GLOAD(min(cur + PD, nst - 1), rb[u]);
+            compute(u & 1);
+            if (cur + 1 < nst) { NLD_TILE_LSTORE(rb[(u + 1) % PD], (u + 1) & 1); }
+            __syncthreads();
+        }
     }
 #undef NLD_TILE_GLOAD
 #undef NLD_TILE_LSTORE
+
+    if (ksplit > 1) {
+        // slice partials, 16 pairs of floats per thread, pair-major so that every store is one
+        // contiguous 512-byte run per wavefront
+        typedef unsigned long long u64;
+        __shared__ int last_s;
+        const int grp = c * R + rg;
+        u64* pp = (u64*)part + (size_t)(grp * ksplit + ksl) * 16 * NT + threadIdx.x;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int q = (i * 4 + j) * 2;
+                __hip_atomic_store(pp + (size_t)q * NT, __builtin_bit_cast(u64, f32x2_t{acc[i][j][0], acc[i][j][1]}),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(pp + (size_t)(q + 1) * NT, __builtin_bit_cast(u64, f32x2_t{acc[i][j][2], acc[i][j][3]}),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        // every lane's stores are acknowledged before the workgroup counts itself in
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            last_s = __hip_atomic_fetch_add(ctr + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(ksplit - 1);
+        __syncthreads();
+        if (!last_s) return;
+        if (threadIdx.x == 0) __hip_atomic_exchange(ctr + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        f32x4_t sum[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sum[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int sl = 0; sl < ksplit; ++sl) {   // fixed order over the slices
+            if (sl == ksl) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) sum[i][j] += acc[i][j];
+                continue;
+            }
+            const u64* qq = (const u64*)part + (size_t)(grp * ksplit + sl) * 16 * NT + threadIdx.x;
+            f32x2_t v[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                v[q] = __builtin_bit_cast(f32x2_t, __hip_atomic_load(qq + (size_t)q * NT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int q = (i * 4 + j) * 2;
+                    sum[i][j] += f32x4_t{v[q][0], v[q][1], v[q + 1][0], v[q + 1][1]};
+                }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = sum[i][j];
+    }
 
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -1303,16 +1376,24 @@ bool gemm_tile_supported(int M, int K, int ksteps) {
 
 int gemm_tile_row_pad() { return tile::BR * 16; }
 
-hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s) {
+int gemm_tile_groups(int M, int n_tiles) { return ((M + tile::BR * 16 - 1) / (tile::BR * 16)) * gemm_tile_parts(n_tiles); }
+int gemm_tile_stages(int ksteps) { return ksteps / tile::KS; }
+size_t gemm_tile_part_floats_per_wg() { return (size_t)tile::NT * 32; }
+int gemm_tile_wgs_per_cu() { return 2; }
+
+hipError_t launch_gemm_tile(int epi, const GemmArgs& a, int ksplit, float* part, unsigned* ctr, hipStream_t s) {
     if (!gemm_tile_supported(a.M, a.K, a.ksteps) || a.W2) return hipErrorInvalidValue;
+    // every slice gets at least one stage; the LM head's argmax partials are per column group
+    if (ksplit < 1 || ksplit > gemm_tile_stages(a.ksteps) || (ksplit > 1 && (!part || !ctr || epi == EPI_LMHEAD)))
+        return hipErrorInvalidValue;
     const int R = (a.M + tile::BR * 16 - 1) / (tile::BR * 16);
     const int C = gemm_tile_parts(a.n_tiles);
-    const dim3 grid((unsigned)(R * ((C + 7) / 8) * 8)), blk(tile::NT);
+    const dim3 grid((unsigned)(R * ((C + 7) / 8) * 8), (unsigned)ksplit), blk(tile::NT);
     switch (epi) {
-        case EPI_QKV: launch(gemm_tile_kernel<EPI_QKV>, grid, blk, s, a, R, C); break;
-        case EPI_RESID: launch(gemm_tile_kernel<EPI_RESID>, grid, blk, s, a, R, C); break;
-        case EPI_SWIGLU: launch(gemm_tile_kernel<EPI_SWIGLU>, grid, blk, s, a, R, C); break;
-        case EPI_LMHEAD: launch(gemm_tile_kernel<EPI_LMHEAD>, grid, blk, s, a, R, C); break;
+        case EPI_QKV: launch(gemm_tile_kernel<EPI_QKV>, grid, blk, s, a, R, C, ksplit, part, ctr); break;
+        case EPI_RESID: launch(gemm_tile_kernel<EPI_RESID>, grid, blk, s, a, R, C, ksplit, part, ctr); break;
+        case EPI_SWIGLU: launch(gemm_tile_kernel<EPI_SWIGLU>, grid, blk, s, a, R, C, ksplit, part, ctr); break;
+        case EPI_LMHEAD: launch(gemm_tile_kernel<EPI_LMHEAD>, grid, blk, s, a, R, C, ksplit, part, ctr); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -278,11 +278,18 @@ hipError_t launch_gemm_splitk(int epi, int ct, int ksplit, const GemmArgs& a, fl
 // Tiled GEMM for M > 64 (no second source): 128 x 128 output tiles.  Needs K % 32 == 0, an
 // even k-step count and the A operand allocated for rows up to a multiple of
 // gemm_tile_row_pad().  gemm_tile_parts gives the number of column groups (the argmax
-// partials per row of the LM head).
+// partials per row of the LM head).  ksplit > 1 (not for the LM head) cuts K into that many
+// slices of whole stages (at most gemm_tile_stages): `part` holds gemm_tile_part_floats_per_wg()
+// floats per (tile group, slice) and `ctr` one counter per tile group (gemm_tile_groups), zero
+// before the launch and zero again after it.
 bool gemm_tile_supported(int M, int K, int ksteps);
 int gemm_tile_row_pad();
 int gemm_tile_parts(int n_tiles);
-hipError_t launch_gemm_tile(int epi, const GemmArgs& a, hipStream_t s);
+int gemm_tile_groups(int M, int n_tiles);
+int gemm_tile_stages(int ksteps);
+size_t gemm_tile_part_floats_per_wg();
+int gemm_tile_wgs_per_cu();   // workgroups of the tiled GEMM resident per CU
+hipError_t launch_gemm_tile(int epi, const GemmArgs& a, int ksplit, float* part, unsigned* ctr, hipStream_t s);
 // kh: key halves per stage (2 when the unit has at most 4 row tiles, else 1); 8 wavefronts per workgroup.
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int head_dim, int units, int rows, const AttnArgs& a, hipStream_t s);

@@ -401,6 +401,36 @@ def test_8b_layer_batched_block_pass(R, layer8b_b4, mode):
     assert R.read_device_status(ws) == 0
 
 
+def test_8b_layer_tile_gemm_k_slices(R, layer8b_b4, monkeypatch):
+    """The tiled GEMM with K slices (by default at 128 rows: O and down 8 slices, QKV 5, met through the
+    workspace by the last-arriving workgroup) against the same GEMM unsliced: both within tolerance of
+    the oracle, equal up to the fp32 rounding of the slice sums, and the sliced result bit-identical over
+    repeated passes whatever order the slices finish in."""
+    t = layer8b_b4
+    shape, k = t["shape"], 32
+    tok = torch.from_numpy(synth_tokens(shape, t["seed"], "8b_layer.b4.kslices", (4, k))).cuda()
+    ref, _, _ = O.block_forward(t["w"], t["okv"], tok.cpu().numpy(), O.DRAFT)
+    out = {}
+    for ks in ("1", None):
+        for kind in ("O", "DOWN", "QKV"):
+            if ks is None:
+                monkeypatch.delenv("NLD_TILE_KSPLIT_" + kind, raising=False)
+            else:
+                monkeypatch.setenv("NLD_TILE_KSPLIT_" + kind, ks)
+        ws = R.Workspace(t["model"], 4, k, t["cache"].max_len)
+        runs = [R.block_forward(t["model"], t["cache"], ws, tok, R.DRAFT)[0].cpu().numpy() for _ in range(3)]
+        assert R.read_device_status(ws) == 0
+        e = rel_err(runs[0], ref)
+        log("8b_layer batch 4 k=32 tile GEMM %s: rel err %.3e" % ("unsliced" if ks else "K slices", e))
+        assert e <= TOL
+        for r in runs[1:]:
+            assert np.array_equal(r, runs[0])
+        out[ks] = runs[0]
+    d = rel_err(out[None], out["1"])
+    log("  sliced vs unsliced: %.3e" % d)
+    assert d < 1e-4
+
+
 # ----------------------------------------------------------------------------- split-K residual GEMM
 @pytest.mark.parametrize("ksplit,ct", [(1, 4), (2, 2), (3, 4), (8, 4), (8, 2)])
 def test_tiny_split_k_residual_gemm(R, tiny, monkeypatch, ksplit, ct):
