@@ -95,6 +95,7 @@ namespace {
 // ---------------------------------------------------------------- workspace layout
 struct Layout {
     int M, Mpad, units, n_splits, chunk, row_tiles, attn_kh, attn_z, n_parts, rows_pad, lm_tiles, lm_parts;
+    bool attn_items;         // length-aware attention work (batches)
     int n_sk_ctr, sk_ctr0;   // split-K residual GEMM: counters (one per column group) from tile counter sk_ctr0
     int n_nk_ctr, nk_ctr0;   // normed GEMM of 17..64 rows: counters (one per column tile) from tile counter nk_ctr0
     int n_tk_ctr, tk_ctr0;   // tiled GEMM with K slices (M > 64): counters (one per tile group) from tk_ctr0
@@ -123,8 +124,15 @@ Layout make_layout(const nld_config& c, int batch, int k, int max_len, int quad_
     // workgroup per CU while there are few (unit, row slice) pairs (batch 1: each workgroup
     // is then a short latency chain); up to four per CU when there are many, so that long
     // and ragged key ranges are cut finer than one per CU.
+    // With more than one sequence the workgroups take length-aware items (only splits holding
+    // committed keys get a workgroup), so the splits may be cut finer: with one row slice the plan
+    // aims at NLD_ATTN_ITEMS_FINER (default 2) times as many workgroups as it would at max_len.
+    // (Measured: 8B batch 32, ragged prefixes, one slice: 198 us against 214 us at 1x and 254 us
+    // without items; 14B batch 8, equal prefixes, two slices: 2x 366 us against 341 us at 1x.)
+    L.attn_items = batch > 1 && !env_int("NLD_ATTN_NO_ITEMS", 0);
     const int pairs = L.units * L.attn_z;
-    const int target = env_int("NLD_ATTN_TARGET_WG", device_cus() * std::min(4, std::max(1, pairs / 16)));
+    const int finer = L.attn_items ? env_int("NLD_ATTN_ITEMS_FINER", L.attn_z == 1 ? 2 : 1) : 1;
+    const int target = env_int("NLD_ATTN_TARGET_WG", finer * device_cus() * std::min(4, std::max(1, pairs / 16)));
     int ns = target / (L.units * L.attn_z) - 1;    // one workgroup per (unit, row slice) is the block part
     const int max_splits = cdiv(max_len, 64);
     if (ns > max_splits) ns = max_splits;
@@ -555,6 +563,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.row_tiles = L.row_tiles;
         at_.quad_k = io.quad_k;
         at_.n_parts = L.n_parts;
+        at_.items = L.attn_items ? 1 : 0;
+        at_.n_seq = batch;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);

@@ -1438,6 +1438,52 @@ __device__ __forceinline__ int stage_key(int tau, int rho) {
     return 32 * (tau >> 1) + 8 * (rho >> 2) + 4 * (tau & 1) + (rho & 3);
 }
 
+// committed length of sequence b as the attention reads it: clamped to [0, max_len]
+__device__ __forceinline__ int attn_length(const AttnArgs& a, int b) {
+    const int p = a.lengths[b];
+    return p < 0 ? 0 : (p > a.max_len ? a.max_len : p);
+}
+
+// Length-aware work item `item` -> (unit, split), split == n_splits for the block part; false past
+// the last item.  Wavefront 0 scans the sequences' item counts (nkv * (ceil(P_b / chunk) + 1)) 64
+// at a time; the result goes to every thread through LDS.
+__device__ bool attn_item(const AttnArgs& a, int item, int* unit, int* split) {
+    __shared__ int su_s, ss_s;
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int base = 0, su = -1, ss = 0;
+        for (int b0 = 0; b0 < a.n_seq && su < 0; b0 += 64) {
+            const int b = b0 + lane;
+            const int nc = b < a.n_seq ? (attn_length(a, b) + a.chunk - 1) / a.chunk : 0;
+            const int cnt = b < a.n_seq ? (nc + 1) * a.n_kv_heads : 0;
+            int incl = cnt;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int t = __shfl_up(incl, off);
+                if (lane >= off) incl += t;
+            }
+            const int excl = incl - cnt;
+            const bool mine = cnt > 0 && item >= base + excl && item < base + incl;
+            const unsigned long long who = __ballot(mine);
+            if (who) {
+                const int src = __ffsll((long long)who) - 1;
+                const int r = __shfl(item - base - excl, src), ncs = __shfl(nc, src);
+                su = (b0 + src) * a.n_kv_heads + r / (ncs + 1);
+                ss = r % (ncs + 1) == ncs ? a.n_splits : r % (ncs + 1);
+            }
+            base += __shfl(incl, 63);
+        }
+        if (lane == 0) {
+            su_s = su;
+            ss_s = ss;
+        }
+    }
+    __syncthreads();
+    *unit = su_s;
+    *split = ss_s;
+    return su_s >= 0;
+}
+
 template <int D, int KH>
 __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     typedef AttnCfg<D> C;
@@ -1453,7 +1499,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
-    const int split = blockIdx.x, unit = blockIdx.y;
+    int split = blockIdx.x, unit = blockIdx.y;
+    if (a.items && !attn_item(a, blockIdx.x, &unit, &split)) return;   // the whole workgroup leaves
     const bool blockpart = split == a.n_splits;   // the block's own keys, read in split form
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv;
@@ -1728,12 +1775,15 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     const int unit = blockIdx.x, rw = blockIdx.y, d = threadIdx.x;
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv, k = a.k_blk;
-    const int ns = a.n_parts;
-    const size_t ubase = (size_t)unit * ns * a.rows_pad + rw;
+    // parts: prefix splits 0 .. nvalid-1 (the ones holding committed keys), then the block part
+    const int nvalid = a.items ? (attn_length(a, b) + a.chunk - 1) / a.chunk : a.n_splits;
+    const int ns = nvalid + 1;
+    auto pidx = [&](int j) { return j < nvalid ? j : a.n_splits; };
+    const size_t ubase = (size_t)unit * a.n_parts * a.rows_pad + rw;
     // split statistics -> weights exp2(m_s - max) in LDS (ns <= 256)
     float ms = -INFINITY, ls = 0.f;
     for (int sp = d; sp < ns; sp += D) {
-        const float2 ml = *(const float2*)(a.part_ml + (ubase + (size_t)sp * a.rows_pad) * 2);
+        const float2 ml = *(const float2*)(a.part_ml + (ubase + (size_t)pidx(sp) * a.rows_pad) * 2);
         wsh[sp] = ml.x;
         ms = fmaxf(ms, ml.x);
     }
@@ -1751,7 +1801,7 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     for (int sp = d; sp < ns; sp += D) {
         const float msp = wsh[sp];
         const float w = (msp == -INFINITY) ? 0.f : exp2f(msp - mx);
-        ls += w * a.part_ml[(ubase + (size_t)sp * a.rows_pad) * 2 + 1];
+        ls += w * a.part_ml[(ubase + (size_t)pidx(sp) * a.rows_pad) * 2 + 1];
         wsh[sp] = w;
     }
     ls += __shfl_xor(ls, 32);
@@ -1770,17 +1820,18 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     for (; sp + 8 <= ns; sp += 8) {
         float os[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) os[e] = a.part_o[(ubase + (size_t)(sp + e) * a.rows_pad) * D + d];
+        for (int e = 0; e < 8; ++e) os[e] = a.part_o[(ubase + (size_t)pidx(sp + e) * a.rows_pad) * D + d];
 #pragma unroll
         for (int e = 0; e < 8; ++e) num += wsh[sp + e] * os[e];
     }
-    for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)sp * a.rows_pad) * D + d];
+    for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)pidx(sp) * a.rows_pad) * D + d];
     const int hl = rw / k, j = rw % k;
     store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den);
 }
 
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
-    const dim3 grid(a.n_splits + 1, units, zslices);   // prefix splits + the block part
+    // prefix splits + the block part per unit; length-aware items: all of them on x
+    const dim3 grid = a.items ? dim3((a.n_splits + 1) * units, 1, zslices) : dim3(a.n_splits + 1, units, zslices);
     if (head_dim == 128 && kh == 2) launch(attention_kernel<128, 2>, dim3(grid), dim3(512), s, a);
     else if (head_dim == 128 && kh == 1) launch(attention_kernel<128, 1>, dim3(grid), dim3(512), s, a);
     else if (head_dim == 64 && kh == 2) launch(attention_kernel<64, 2>, dim3(grid), dim3(512), s, a);

@@ -163,6 +163,11 @@ struct AttnArgs {
     int quad_k;          // mode 2 (quadratic self-speculation): chain length of the block's layout
     int n_parts;         // partial results per (unit, row): n_splits prefix splits + the block part
     float scale_log2;    // log2(e) / sqrt(D)
+    // Length-aware work (batches): grid.x counts (unit, split) items numbered unit by unit from the
+    // committed lengths, unit u of sequence b taking ceil(P_b / chunk) prefix splits and the block
+    // part; items past the total leave at once, and the merge reads only the valid parts.
+    int items;
+    int n_seq;           // sequences (units / n_kv_heads)
 };
 
 struct EmbedArgs {

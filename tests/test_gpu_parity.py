@@ -318,6 +318,46 @@ def test_bad_token_is_reported(R, tiny):
 
 
 # ----------------------------------------------------------------------------- one 8B-shaped layer + LM head
+@pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
+def test_tiny_ragged_batch_attention_items(R, monkeypatch, mode):
+    """A ragged batch (committed lengths 0, 70, 128, 1 and 248: an empty prefix, one key, split boundaries
+    and a block that ends at max_len) with the attention's length-aware work items (the default for
+    batches: only splits holding committed keys get a workgroup, the merge reads only those) and with
+    the plain grid over max_len: both within tolerance of the oracle and equal up to the fp32
+    rounding of the merge."""
+    wl = WORKLOADS["tiny"]
+    shape, seed = wl.shape, wl.seed
+    lengths = np.array([0, 70, 128, 1, 256 - 8])
+    B, k, max_len = len(lengths), 8, 256
+    src = LazyWeights(shape, seed)
+    w = O.OracleWeights(shape, src, np.float32)
+    okv = O.OracleKV(shape, B, max_len, np.float32)
+    model = R.DeviceModel(shape, src)
+    cache = R.DeviceCache(shape, B, max_len)
+    for l in range(shape.n_layers):
+        kb, vb = prefix_kv(shape, seed, l, B, int(lengths.max()))
+        okv.set_prefix_bf16(l, kb, vb, lengths)
+        cache.load_prefix(l, kb, vb)
+    cache.set_lengths(lengths)
+    tok = synth_tokens(shape, seed, "tiny.ragged", (B, k))
+    ref, _, _ = O.block_forward(w, okv, tok, mode)
+    out = {}
+    for items in ("1", "0"):
+        monkeypatch.setenv("NLD_ATTN_NO_ITEMS", "0" if items == "1" else "1")
+        ws = R.Workspace(model, B, k, max_len)
+        logits, am = R.block_forward(model, cache, ws, torch.from_numpy(tok).cuda(),
+                                     R.VERIFY if mode == O.VERIFY else R.DRAFT)
+        g = logits.cpu().numpy()
+        e = rel_err(g, ref)
+        log("tiny ragged batch %s, %s: rel err %.3e" % (mode, "items" if items == "1" else "grid", e))
+        assert e <= TOL
+        check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+        assert R.read_device_status(ws) == 0
+        out[items] = g
+    assert rel_err(out["1"], out["0"]) < 1e-5
+    assert cache.lengths.cpu().numpy().tolist() == lengths.tolist()
+
+
 @pytest.fixture(scope="module")
 def layer8b(R):
     wl = WORKLOADS["8b_layer"]
