@@ -241,7 +241,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     if (cur < T) {
         const uint4* p = a.W + ((size_t)cur * a.ksteps + s0) * 64 + lane;
 #pragma unroll
-        for (int s = 0; s < KS; ++s) wb[s] = p[(size_t)s * 64];
+        for (int s = 0; s < KS; ++s) wb[s] = load_stream(p + (size_t)s * 64);
     }
 
     // operand slice: row r, columns 32*(s0+s) + 8g .. +8, hi and lo
@@ -277,7 +277,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
         for (int s = 0; s < KS; ++s) {
             acc = mfma_16x16x32(ah[s], wb[s], acc);
             accl = mfma_16x16x32(al[s], wb[s], accl);
-            if (more) wb[s] = p[(size_t)s * 64];
+            if (more) wb[s] = load_stream(p + (size_t)s * 64);
         }
         if (threadIdx.x == 0) next_s[(it + 1) & 1] = nxt < T ? min(G + (int)grab, T) : T;
         const int parity = it & 1;

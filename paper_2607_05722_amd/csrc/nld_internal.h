@@ -33,6 +33,15 @@ __device__ __forceinline__ f32x4_t mfma_16x16x32(uint4 a, uint4 b, f32x4_t c) {
                                                    c, 0, 0, 0);
 }
 
+// One 16-byte block of a weight matrix that is read once per pass: a non-temporal load, so that
+// the stream does not displace the lines that are reused from L2 (the split operand every
+// workgroup reads, the residual rows).
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+    typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+    const u32x4_nt v = __builtin_nontemporal_load((const u32x4_nt*)p);
+    return uint4{v[0], v[1], v[2], v[3]};
+}
+
 // Order-preserving key for a float value at column n: larger value wins, then
 // lower column.  -0.0 is folded onto +0.0 so that equal values tie on index.
 __device__ __forceinline__ unsigned long long argmax_key(float v, uint32_t n) {
