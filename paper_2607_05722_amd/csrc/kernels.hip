@@ -1780,12 +1780,29 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     const int ns = nvalid + 1;
     auto pidx = [&](int j) { return j < nvalid ? j : a.n_splits; };
     const size_t ubase = (size_t)unit * a.n_parts * a.rows_pad + rw;
+    // With at most FAST parts every load of the workgroup is issued at once: thread d's part
+    // statistics and its column of every part's output.  More parts take the looped path.
+    constexpr int FAST = 32;
+    const bool fast = ns <= FAST;
+    float2 ml0 = float2{-INFINITY, 0.f};
+    float os[FAST];
+    if (fast) {
+        if (d < ns) ml0 = *(const float2*)(a.part_ml + (ubase + (size_t)pidx(d) * a.rows_pad) * 2);
+#pragma unroll
+        for (int e = 0; e < FAST; ++e)
+            os[e] = e < ns ? a.part_o[(ubase + (size_t)pidx(e) * a.rows_pad) * D + d] : 0.f;
+    }
     // split statistics -> weights exp2(m_s - max) in LDS (ns <= 256)
     float ms = -INFINITY, ls = 0.f;
-    for (int sp = d; sp < ns; sp += D) {
-        const float2 ml = *(const float2*)(a.part_ml + (ubase + (size_t)pidx(sp) * a.rows_pad) * 2);
-        wsh[sp] = ml.x;
-        ms = fmaxf(ms, ml.x);
+    if (fast) {
+        if (d < ns) wsh[d] = ml0.x;
+        ms = ml0.x;
+    } else {
+        for (int sp = d; sp < ns; sp += D) {
+            const float2 ml = *(const float2*)(a.part_ml + (ubase + (size_t)pidx(sp) * a.rows_pad) * 2);
+            wsh[sp] = ml.x;
+            ms = fmaxf(ms, ml.x);
+        }
     }
     // block max over D threads (D <= 128: two wavefronts at most)
     ms = fmaxf(ms, __shfl_xor(ms, 32));
@@ -1798,11 +1815,19 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     if ((d & 63) == 0) wmax[d >> 6] = ms;
     __syncthreads();
     const float mx = (D > 64) ? fmaxf(wmax[0], wmax[1]) : wmax[0];
-    for (int sp = d; sp < ns; sp += D) {
-        const float msp = wsh[sp];
-        const float w = (msp == -INFINITY) ? 0.f : exp2f(msp - mx);
-        ls += w * a.part_ml[(ubase + (size_t)pidx(sp) * a.rows_pad) * 2 + 1];
-        wsh[sp] = w;
+    if (fast) {
+        if (d < ns) {
+            const float w = (ml0.x == -INFINITY) ? 0.f : exp2f(ml0.x - mx);
+            ls = w * ml0.y;
+            wsh[d] = w;
+        }
+    } else {
+        for (int sp = d; sp < ns; sp += D) {
+            const float msp = wsh[sp];
+            const float w = (msp == -INFINITY) ? 0.f : exp2f(msp - mx);
+            ls += w * a.part_ml[(ubase + (size_t)pidx(sp) * a.rows_pad) * 2 + 1];
+            wsh[sp] = w;
+        }
     }
     ls += __shfl_xor(ls, 32);
     ls += __shfl_xor(ls, 16);
@@ -1815,16 +1840,23 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     __syncthreads();
     if (d == 0) inv_den = 1.0f / ((D > 64) ? (wden[0] + wden[1]) : wden[0]);
     __syncthreads();
+    // the parts in order, one product-sum each (the same order on both paths)
     float num = 0.f;
-    int sp = 0;
-    for (; sp + 8 <= ns; sp += 8) {
-        float os[8];
+    if (fast) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) os[e] = a.part_o[(ubase + (size_t)pidx(sp + e) * a.rows_pad) * D + d];
+        for (int e = 0; e < FAST; ++e)
+            if (e < ns) num += wsh[e] * os[e];
+    } else {
+        int sp = 0;
+        for (; sp + 8 <= ns; sp += 8) {
+            float o8[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) num += wsh[sp + e] * os[e];
+            for (int e = 0; e < 8; ++e) o8[e] = a.part_o[(ubase + (size_t)pidx(sp + e) * a.rows_pad) * D + d];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) num += wsh[sp + e] * o8[e];
+        }
+        for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)pidx(sp) * a.rows_pad) * D + d];
     }
-    for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)pidx(sp) * a.rows_pad) * D + d];
     const int hl = rw / k, j = rw % k;
     store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den);
 }
