@@ -439,7 +439,7 @@ __global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part
     for (int p = 0; p < PF; ++p) {
 #pragma unroll
         for (int s = 0; s < KS; ++s)
-            wb[p][s] = a.W[((size_t)min(x + p * Gx, T - 1) * a.ksteps + min(s0 + s, s_last)) * 64 + lane];
+            wb[p][s] = load_stream(a.W + ((size_t)min(x + p * Gx, T - 1) * a.ksteps + min(s0 + s, s_last)) * 64 + lane);
         store_part(x, f32x4_t{0.f, 0.f, 0.f, 0.f});
     }
 
@@ -482,7 +482,7 @@ __global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part
                 acc[mt] = mfma_16x16x32(ah[mt][s], w[s], acc[mt]);
                 acc[mt] = mfma_16x16x32(al[mt][s], w[s], acc[mt]);
             }
-            w[s] = a.W[((size_t)tn * a.ksteps + min(s0 + s, s_last)) * 64 + lane];
+            w[s] = load_stream(a.W + ((size_t)tn * a.ksteps + min(s0 + s, s_last)) * 64 + lane);
         }
         const int par = j & 1;
 #pragma unroll
