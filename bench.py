@@ -435,15 +435,21 @@ def main():
         len0 = cache.lengths.clone()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        # one event between consecutive steps: the whole region gives the mean, the pairs the percentiles
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps - 1)]
         e0.record()
-        for _ in range(steps):
+        for i in range(steps):
             if graph is not None:
                 graph.replay()
             else:
                 step()
+            if i < steps - 1:
+                marks[i].record()
         e1.record()
         torch.cuda.synchronize()
         elapsed_ms = e0.elapsed_time(e1)
+        bounds = [e0] + marks + [e1]
+        per_step = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(steps)])
         committed = int((cache.lengths - len0).sum().item())
         status = R.read_device_status(ws)
 
@@ -491,6 +497,9 @@ def main():
         "steps": steps,
         "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "step_ms_percentiles": {"p10": round(float(np.percentile(per_step, 10)), 4),
+                                "p50": round(float(np.percentile(per_step, 50)), 4),
+                                "p90": round(float(np.percentile(per_step, 90)), 4)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
