@@ -371,6 +371,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--max-len", type=int, default=0,
+                    help="KV cache capacity in positions (default: the prefix plus the steps' growth)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the Mode 2 and LoRA timings (counter runs use this: eager launches only)")
@@ -393,6 +395,10 @@ def main():
     plens = wl.prefix_lengths()
     steps, warmup = args.steps, args.warmup
     max_len = int(-(-(int(plens.max()) + (steps + warmup + 6) * k) // 64) * 64)
+    if args.max_len:
+        if args.max_len < max_len or args.max_len % 64:
+            sys.exit("--max-len must be a multiple of 64 and at least %d" % max_len)
+        max_len = args.max_len
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
@@ -510,7 +516,7 @@ def main():
                                % (wl.name, shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads,
                                   shape.head_dim, shape.ffn, shape.vocab, B,
                                   int(plens[0]) if wl.ragged is None else "ragged %d..%d" % wl.ragged, k),
-                   "graph": graph is not None},
+                   "graph": graph is not None, "kv_capacity": max_len},
         "pass_ms": round(ms_per_step / 2, 4),
         "step_hbm_GBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
         "step_hbm_frac": round(bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

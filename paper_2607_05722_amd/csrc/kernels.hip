@@ -1521,7 +1521,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const bool bidir_row = (a.mode == 1) && (j >= a.bidir_from);
     const int grp = (quad && j >= qk) ? (j - qk) / qk : j;
     const int lo_c = (quad && j >= qk) ? qk + grp * qk : k, hi_c = (quad && j >= qk) ? lo_c + qk : k;
-    const int split_beg = split * a.chunk;   // prefix splits: first key of the split (< max_len)
+    int split_beg = split * a.chunk;   // prefix splits: first key of the split (< max_len)
 
     const size_t head_off = (size_t)(b * nkv + kvh) * a.max_len * D;
     const uint16_t* kbase = a.kc + head_off;   // where gload reads stages from
@@ -1606,9 +1606,23 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     }
 
     int P = P_raw < 0 ? 0 : (P_raw > a.max_len ? a.max_len : P_raw);
+    // One sequence: the n_splits prefix splits are cut from the committed length, chunk =
+    // ceil(P / n_splits) rounded up to whole stages (at most the plan's chunk, which was cut from
+    // max_len), so that a cache much longer than its prefix still spreads the prefix over every
+    // split.  The first stage went out at the plan's split start; it is requested again where
+    // the two differ.
+    int chunk = a.chunk;
+    if (!a.items && !blockpart) {
+        chunk = max(64, ((P + a.n_splits - 1) / a.n_splits + 63) / 64 * 64);
+        const int beg = split * chunk;
+        if (beg != split_beg) {
+            split_beg = beg;
+            if (beg < P) s0 = gload(beg);   // beg < P <= max_len, a multiple of 64: inside the cache
+        }
+    }
     // prefix splits cover committed keys [kbeg, kend) of [0, P); the block part covers [P, P + k)
     const int kbeg = blockpart ? P : split_beg;
-    const int kend = blockpart ? P + k : min(kbeg + a.chunk, P);
+    const int kend = blockpart ? P + k : min(kbeg + chunk, P);
     const int nst = blockpart ? 1 : (kend > kbeg ? (kend - kbeg + 63) / 64 : 0);
     if (!blockpart) {
         if (nst > 1) s1 = gload(kbeg + 64);

@@ -399,6 +399,40 @@ def test_8b_layer_block_pass(R, layer8b, k, mode):
     assert R.read_device_status(ws) == 0
 
 
+@pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
+def test_8b_layer_long_cache_block_pass(R, layer8b, mode):
+    """A cache whose capacity (16384) is eight times its committed prefix (2048): one sequence's prefix
+    splits are cut from the committed length on the device, not from the capacity.  Within tolerance of
+    the oracle, and equal to the same pass over a cache of capacity 2112 up to the fp32 rounding of the
+    merge (the split boundaries differ)."""
+    t = layer8b
+    shape, k = t["shape"], 16
+    P = 2048
+    cache = R.DeviceCache(shape, 1, 16384)
+    kb, vb = prefix_kv(shape, t["seed"], 0, 1, P)
+    cache.load_prefix(0, kb, vb)
+    cache.set_lengths([P])
+    tok = synth_tokens(shape, t["seed"], "8b_layer.long%d" % k, (1, k))
+    ref, nk, nv = O.block_forward(t["w"], t["okv"], tok, mode)
+    out = {}
+    for name, c in (("long", cache), ("short", t["cache"])):
+        ws = R.Workspace(t["model"], 1, k, c.max_len)
+        logits, am = R.block_forward(t["model"], c, ws, torch.from_numpy(tok).cuda(),
+                                     R.VERIFY if mode == O.VERIFY else R.DRAFT)
+        g = logits.cpu().numpy()
+        e = rel_err(g, ref)
+        log("8b_layer %s cache (capacity %d) k=%d %s: rel err %.3e" % (name, c.max_len, k, mode, e))
+        assert e <= TOL
+        check_argmax(am.cpu().numpy(), g, ref, e * np.max(np.abs(ref)))
+        assert R.read_device_status(ws) == 0
+        out[name] = g
+    assert rel_err(out["long"], out["short"]) < 1e-5
+    if mode == O.VERIFY:
+        kg, vg = cache.read_kv(0, P, P + k)
+        assert rel_err(O.bf16_bits_to_float(kg), nk[0]) < TOL
+        assert rel_err(O.bf16_bits_to_float(vg), nv[0]) < TOL
+
+
 @pytest.fixture(scope="module")
 def layer8b_b4(R):
     """One 8B-shaped layer, batch 4 with ragged prefixes: 128 block rows at k=32 (the tiled GEMM path)."""
