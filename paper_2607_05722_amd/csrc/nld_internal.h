@@ -33,9 +33,9 @@ __device__ __forceinline__ f32x4_t mfma_16x16x32(uint4 a, uint4 b, f32x4_t c) {
                                                    c, 0, 0, 0);
 }
 
-// One 16-byte block of a weight matrix that is read once per pass: a non-temporal load, so that
-// the stream does not displace the lines that are reused from L2 (the split operand every
-// workgroup reads, the residual rows).
+// One 16-byte block of a weight matrix that is read once per pass, loaded with the non-temporal
+// hint (the `nt` bit).  The normed GEMMs use it for their weight streams, where it measured
+// faster; the O, down and attention streams measured slower with it and keep plain loads.
 __device__ __forceinline__ uint4 load_stream(const uint4* p) {
     typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
     const u32x4_nt v = __builtin_nontemporal_load((const u32x4_nt*)p);
