@@ -1,6 +1,6 @@
 """Benchmark of the block-decode step (draft pass + verify pass + acceptance) on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload 8b] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload 8b] [--max-len L] [--no-cpu-baseline]
 
 A step is one linear self-speculation step over the synthetic workload: the
 diffusion draft pass over [anchor, mask x (k-1)], the causal verify pass over
