@@ -16,7 +16,8 @@ Also timed (not part of value), each replayed from its own captured graph:
 and without the LoRA-enhanced drafter's adapter (rank 128) on the O projection;
 "quad_ss" -- one quadratic self-speculation step (chain length 7, 56 block rows)
 with the AR verifier and with the lambda = 0.5 ensemble, beside one linear step
-(draft + verify) of the same speculative width.
+(draft + verify) of the same speculative width; "block_k32" -- one linear step
+at block size 32 (the paper's main block length) over the same prefix.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -208,6 +209,30 @@ def quad_timing(R, model, cache, anchor, reps):
     cache.lengths.copy_(len0)
     torch.cuda.synchronize()
     return res
+
+
+def block_size_timing(R, model, cache, anchor, reps, k):
+    """Mean ms of one linear self-speculation step (draft + verify + accept) at block size k, replayed from a
+    captured graph with the lengths reset first, so that every replay runs over the same prefix."""
+    import torch
+    B, dev = anchor.shape[0], anchor.device
+    ws = R.Workspace(model, B, k, cache.max_len)
+    a0 = anchor.clone()
+    len0 = cache.lengths.clone()
+    i32 = lambda *shp: torch.empty(shp, dtype=torch.int32, device=dev)
+    outs = {"accept_len": i32(B), "committed": i32(B, k), "next_anchor": i32(B)}
+    d = i32(B, k - 1)
+
+    def linear():
+        cache.lengths.copy_(len0)
+        R.draft(model, cache, ws, a0, k, out=d)
+        R.verify_accept(model, cache, ws, a0, d, k, outs=outs)
+
+    ms = graph_ms(linear, reps)
+    status = R.read_device_status(ws)
+    cache.lengths.copy_(len0)
+    torch.cuda.synchronize()
+    return ms, status
 
 
 def blas_threads():
@@ -472,12 +497,14 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
-        m2_ms = lora_ms = quad_ms = layer_ms = None
+        m2_ms = lora_ms = quad_ms = layer_ms = k32_ms = None
         if not args.no_extras:
             block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
             m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
             lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
             quad_ms = quad_timing(R, model, cache, anchor, max(5, steps // 2))
+            k32_ms, k32_status = block_size_timing(R, model, cache, anchor, max(5, steps // 2), 32)
+            status |= k32_status
             layer_ms = layer_microbench(R)
             status |= R.read_device_status(ws) | lora_ms["status"] | quad_ms["status"]
 
@@ -555,6 +582,12 @@ def main():
         res["hbm_copy_GBps"] = copy_ceiling()   # what a plain copy reaches on this part (read + write)
         res["hbm_sum_read_GBps"] = read_ceiling()   # and a plain reduction (reads only)
         res["layer_microbench"] = layer_ms
+    if k32_ms is not None:
+        res["block_k32"] = {
+            "step_ms": round(k32_ms, 4),
+            "block_tokens_per_s": round(2.0 * B * 32 / (k32_ms * 1e-3), 1),
+            "hbm_frac": round(2 * pass_bytes(shape, B, 32, plens) / (k32_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
     if quad_ms is not None:
         R_q = QUAD_K * (QUAD_K + 1)
         res["quad_ss"] = {
