@@ -229,10 +229,11 @@ def block_size_timing(R, model, cache, anchor, reps, k):
         R.verify_accept(model, cache, ws, a0, d, k, outs=outs)
 
     ms = graph_ms(linear, reps)
+    kernels = traced_kernels(linear, 3)
     status = R.read_device_status(ws)
     cache.lengths.copy_(len0)
     torch.cuda.synchronize()
-    return ms, status
+    return ms, kernels, status
 
 
 def blas_threads():
@@ -503,7 +504,7 @@ def main():
             m2_ms, m2_committed = mode2_timing(R, model, cache, ws, anchor, block_full, k, max(5, steps // 2))
             lora_ms = lora_timing(R, model, cache, ws, anchor, k, max(5, steps // 2), wl)
             quad_ms = quad_timing(R, model, cache, anchor, max(5, steps // 2))
-            k32_ms, k32_status = block_size_timing(R, model, cache, anchor, max(5, steps // 2), 32)
+            k32_ms, k32_kernels, k32_status = block_size_timing(R, model, cache, anchor, max(5, steps // 2), 32)
             status |= k32_status
             layer_ms = layer_microbench(R)
             status |= R.read_device_status(ws) | lora_ms["status"] | quad_ms["status"]
@@ -587,6 +588,7 @@ def main():
             "step_ms": round(k32_ms, 4),
             "block_tokens_per_s": round(2.0 * B * 32 / (k32_ms * 1e-3), 1),
             "hbm_frac": round(2 * pass_bytes(shape, B, 32, plens) / (k32_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "kernels": k32_kernels,
         }
     if quad_ms is not None:
         R_q = QUAD_K * (QUAD_K + 1)
