@@ -1,6 +1,6 @@
 """Benchmark of the block-decode step (draft pass + verify pass + acceptance) on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload 8b] [--max-len L] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload 8b] [--k 16] [--max-len L] [--no-cpu-baseline]
 
 A step is one linear self-speculation step over the synthetic workload: the
 diffusion draft pass over [anchor, mask x (k-1)], the causal verify pass over
@@ -397,6 +397,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--k", type=int, default=0, help="block size (default: the workload's first)")
     ap.add_argument("--max-len", type=int, default=0,
                     help="KV cache capacity in positions (default: the prefix plus the steps' growth)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -417,7 +418,9 @@ def main():
     if args.copy_calibration_mib:
         copy_calibration(args.copy_calibration_mib)
     wl = WORKLOADS[args.workload]
-    shape, k, B = wl.shape, wl.k_values[0], wl.batch
+    shape, k, B = wl.shape, (args.k or wl.k_values[0]), wl.batch
+    if not 1 <= k <= 64:
+        sys.exit("--k must be in [1, 64]")
     plens = wl.prefix_lengths()
     steps, warmup = args.steps, args.warmup
     max_len = int(-(-(int(plens.max()) + (steps + warmup + 6) * k) // 64) * 64)
@@ -522,7 +525,7 @@ def main():
     dom = max((n for n in kernels), key=lambda n: kernels[n]["avg_us"] * kernels[n]["launches_per_step"])
     dom_avg_s = kernels[dom]["avg_us"] * 1e-6
     achieved = kb[dom] / dom_avg_s / 1e9
-    traffic = measured_traffic(dom) if args.workload == "8b" else None
+    traffic = measured_traffic(dom) if args.workload == "8b" and k == wl.k_values[0] else None
     res = {
         "metric": METRIC,
         "value": round(value, 1),
