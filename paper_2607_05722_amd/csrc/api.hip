@@ -378,15 +378,17 @@ hipError_t tile_gemm(int kind, int epi, const GemmArgs& g, void* ws, const Layou
 // every wavefront (8 per workgroup) getting at least two k-steps.  Defaults per
 // projection (measured on MI355X at the 8B shapes): up to 16 rows down 2 tiles, O off (the
 // streamed GEMM, 11.3 against 12.9 us), QKV and gate/up off (the normed multi-tile kernel is
-// faster there); 17..64 rows every projection 4 tiles.  Environment overrides:
+// faster there); 17..64 rows every projection 4 tiles, except QKV at 17..32 rows, 3 tiles (taken
+// there before the normed multi-tile kernel).  Environment overrides:
 // NLD_SPLITK_<O|DOWN|QKV|GU> = "ct,ksplit" ("ct,0": ksplit from the rule; "0": off),
 // NLD_SPLITK / NLD_SPLITK_CT for every projection at once, NLD_NO_SPLITK = 1: off.
 
 bool plan_splitk(int kind, int epi, const GemmArgs& g, const Layout& L, int* ct, int* ksplit) {
     if (g.W2 || L.n_sk_ctr == 0 || env_int("NLD_NO_SPLITK", 0)) return false;
     static const char* names[] = {"NLD_SPLITK_O", "NLD_SPLITK_DOWN", "NLD_SPLITK_QKV", "NLD_SPLITK_GU"};
-    static const int dflt_ct[2][4] = {{0, 2, 0, 0}, {4, 4, 4, 4}};   // up to 16 rows; 17..64 rows
-    int c = dflt_ct[g.M > 16][kind], ks = 0;
+    // column tiles per workgroup: up to 16 rows; 17..32 rows; 33..64 rows
+    static const int dflt_ct[3][4] = {{0, 2, 0, 0}, {4, 4, 3, 4}, {4, 4, 4, 4}};
+    int c = dflt_ct[g.M <= 16 ? 0 : (g.M <= 32 ? 1 : 2)][kind], ks = 0;
     const char* v = getenv(names[kind]);
     if (v && *v) {
         c = atoi(v);
@@ -445,6 +447,11 @@ hipError_t normed_gemm(int epi, GemmArgs g, void* ws, const Layout& L, hipStream
     g.n_ss = g.K / 16;
     int ks = 0, waves = 0, ct = 0, ksplit = 0;
     hipError_t err = hipSuccess;
+    // QKV of 17..32 rows: the split-K GEMM, 3 column tiles x 2 K slices per workgroup (8B shapes at
+    // k = 32: 23.6 against 25.2 us for the multi-tile kernel)
+    if (epi == EPI_QKV && g.M > 16 && g.M <= 32 && plan_splitk(SK_QKV, epi, g, L, &ct, &ksplit))
+        return launch_gemm_splitk(epi, ct, ksplit, g, at<float>(ws, L.sk_part),
+                                  at<unsigned>(ws, L.tile_ctr) + L.sk_ctr0, s);
     if (try_normk(epi, g, ws, L, s, parts_out, &err)) return err;   // 17..64 rows
     if ((epi == EPI_QKV || (epi == EPI_SWIGLU && g.M > 16)) &&
         plan_splitk(epi == EPI_QKV ? SK_QKV : SK_GU, epi, g, L, &ct, &ksplit))
