@@ -61,7 +61,8 @@ typedef enum {
 
 /* Device status bits (sticky, OR-ed together). */
 #define NLD_DEV_BAD_TOKEN 0x1u     /* a token id outside [0, vocab) was replaced by 0 */
-#define NLD_DEV_CAPACITY 0x2u      /* P_b + k > max_len: the block's K/V rows were not written */
+#define NLD_DEV_CAPACITY 0x2u      /* P_b + k > max_len: the block's K/V rows at or past max_len were not
+                                      written, and a commit that would pass max_len stops the length there */
 #define NLD_DEV_BAD_LENGTH 0x4u    /* a negative committed length was read */
 #define NLD_DEV_MASK_LEFT 0x8u     /* nld_refresh_block found a mask token in block rows 1..k-1 */
 
@@ -125,7 +126,9 @@ typedef struct {
  * [P_b, P_b + k) (a draft pass writes no cache row), and only
  * nld_verify_accept (by L+1: the anchor row and the accepted draft rows) and
  * nld_refresh_block (by k-1) advance lengths, which commits those rows; the
- * rest are overwritten by later passes.
+ * rest are overwritten by later passes.  A length never advances past max_len:
+ * a commit that would (its rows at or past max_len were not written) stops at
+ * max_len and sets NLD_DEV_CAPACITY, so every row below lengths[b] is valid.
  * Within a pass the block attends to its own keys and values from a
  * higher-precision copy in the workspace (bf16 value plus bf16 remainder),
  * so the cache rows are only what a commit keeps. */

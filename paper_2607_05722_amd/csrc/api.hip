@@ -653,6 +653,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     fa.batch = batch;
     fa.finish = io.finish;
     fa.status = status;
+    fa.max_len = kv->max_len;
     fa.mask_id = c.mask_token_id;
     if (io.kv_only) {
         fa.block = io.block;

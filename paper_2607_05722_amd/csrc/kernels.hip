@@ -14,9 +14,30 @@
 // The GEMMs are skinny (M = batch*k rows, usually 8..32): bound by streaming the
 // bf16 weights from HBM.  Weights are pre-packed so that one 16-byte load per
 // lane of a wavefront is exactly one MFMA B operand (1 KiB contiguous per
-// wavefront load).  No kernel communicates across workgroups: every output
-// element is finished by exactly one workgroup (agent-scope fences and
-// same-address atomics cost tens of microseconds per kernel on this chip).
+// wavefront load).
+//
+// Communication between workgroups of one launch.  The normed GEMM hands out
+// tiles from a counter.  The split-K GEMM, the 17..64-row normed GEMM and the
+// tiled GEMM with K slices meet through last-arriver counters; no workgroup ever
+// waits for another.  The protocol of a slice partial:
+//   1. every lane writes its part with agent-scope relaxed atomic stores;
+//   2. s_waitcnt(0): the wavefront waits until each of its stores is
+//      acknowledged, then a workgroup barrier;
+//   3. one thread adds 1 to the counter (agent-scope relaxed fetch_add); the
+//      workgroup that reads ksplit - 1 is the last to arrive;
+//   4. the last arriver resets the counter to 0, reads the other partials with
+//      agent-scope relaxed atomic loads, adds the slices in slice order (so the
+//      sum does not depend on who arrived last) and runs the epilogue.
+// Why this orders the data: agent-scope stores are made visible at agent scope
+// (past the XCD-local L2) by the time they are acknowledged, so after step 2
+// the partials are readable by agent-scope loads from any XCD; the barrier and
+// the data dependence through the counter's value order step 4 after step 3.
+// The C++ memory model would ask for an agent-scope release fence before the
+// fetch_add (an L2 write-back measured at 11-18 us per kernel here); relaxed
+// stores plus the store-acknowledgement wait rely instead on how gfx950
+// completes agent-scope stores.  Repeated passes giving bit-identical results
+// guard it in the tests.  Every counter is back at zero when its kernel ends,
+// and the embedding kernel zeroes all of them at the start of each pass.
 
 #include "nld_internal.h"
 
@@ -1978,6 +1999,18 @@ __device__ __forceinline__ float argmax_key_value(unsigned long long key) {
     return __uint_as_float((ord & 0x80000000u) ? (ord ^ 0x80000000u) : ~ord);
 }
 
+// Commit n more rows of sequence b.  Rows at or past max_len were never written (the QKV epilogue
+// skipped them and set DEV_CAPACITY), so the length stops at max_len: every row below it is valid.
+__device__ __forceinline__ void advance_length(const FinishArgs& a, int b, int n) {
+    const int p = a.lengths[b] + n;
+    if (p > a.max_len) {
+        atomicOr(a.status, DEV_CAPACITY);
+        a.lengths[b] = a.max_len;
+    } else {
+        a.lengths[b] = p;
+    }
+}
+
 __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
     __shared__ int32_t am[64];
     __shared__ float cf[64];
@@ -1990,7 +2023,7 @@ __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
         for (int j = 1; j < k; ++j)
             if (blk[j] == a.mask_id) atomicOr(a.status, DEV_MASK_LEFT);
         a.next_anchor[b] = blk[k - 1];
-        a.lengths[b] += k - 1;
+        advance_length(a, b, k - 1);
         return;
     }
     for (int jr = wave; jr < k; jr += nw) {
@@ -2061,7 +2094,7 @@ __global__ void __launch_bounds__(1024) finish_kernel(FinishArgs a) {
         a.accept_len[b] = L;
         for (int i = 0; i < k; ++i) a.committed[(size_t)b * k + i] = i < L ? dr[i] : (i == L ? am[L] : -1);
         a.next_anchor[b] = am[L];
-        if (a.lengths) a.lengths[b] += L + 1;
+        if (a.lengths) advance_length(a, b, L + 1);
     }
 }
 
@@ -2175,7 +2208,7 @@ __global__ void __launch_bounds__(1024) quad_finish_kernel(FinishArgs a) {
         for (int i = 0; i < qk; ++i) a.committed[(size_t)b * qk + i] = i < L ? sp[i] : (i == L ? v_s[L] : -1);
         a.accept_len[b] = L;
         a.next_anchor[b] = v_s[L];
-        if (a.lengths) a.lengths[b] += L + 1;
+        if (a.lengths) advance_length(a, b, L + 1);
         L_s = L;
     }
     __syncthreads();

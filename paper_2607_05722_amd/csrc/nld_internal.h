@@ -219,6 +219,7 @@ struct FinishArgs {
     int32_t* committed;                   // [batch][k]
     int32_t* next_anchor;
     int32_t* lengths;                     // advanced by L+1 (may be NULL); FINISH_REFRESH: by k-1
+    int max_len;                          // cache capacity: a length never advances past it (DEV_CAPACITY)
     // FINISH_DENOISE: confidence-threshold commit into `block`; FINISH_REFRESH: reads `block`
     const float2* part_lse;               // [M][n_parts] (NULL with `logits`: reduced from them)
     int32_t* block;                       // [batch][k]

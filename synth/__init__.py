@@ -104,3 +104,17 @@ def f32_to_bf16(x: float) -> int:
 def bf16_ones(n: int) -> np.ndarray:
     """bfloat16 bit patterns of 1.0 (0x3F80)."""
     return np.full(n, 0x3F80, dtype=np.uint16)
+
+
+def f32_array_to_bf16(x: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) of float32 values, round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def gain_bf16(seed: int, name: str, n: int, std: float) -> np.ndarray:
+    """bfloat16 bit patterns of 1 + std * z (z standard normal, its own stream): a seeded vector of
+    scale factors near one.  std = 0 gives exact ones."""
+    if std == 0.0:
+        return bf16_ones(n)
+    return f32_array_to_bf16((1.0 + std * normal_f64(seed, name, (n,))).astype(np.float32))

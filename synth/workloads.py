@@ -15,8 +15,10 @@ seeded draw):
 * ``14b``       -- 40 layers, hidden 5120, 40/8 heads, FFN 17408; batch 8,
                    prefix 16384; k=32.
 
-Weights are N(0, 0.02) bfloat16, stored [out_features][in_features]; RMSNorm
-gains are 1.0; the LM head is a separate matrix from the embedding.  The
+Weights are N(0, 0.02) bfloat16, stored [out_features][in_features]; every
+RMSNorm gain vector (each layer's attention and FFN norms, the final norm) is its
+own seeded draw bf16(1 + 0.1 z), so that a gain applied at the wrong place shows
+in the output; the LM head is a separate matrix from the embedding.  The
 mask token is id vocab-1; block and prefix tokens are uniform over
 [0, vocab-2] so they never collide with it.  Nothing here computes any part
 of the forward pass.
@@ -28,7 +30,7 @@ from typing import List, Optional
 
 import numpy as np
 
-from . import normal_bf16, uniform_int, bf16_ones
+from . import gain_bf16, normal_bf16, uniform_int
 
 
 @dataclass(frozen=True)
@@ -45,6 +47,7 @@ class ModelShape:
     init_std: float = 0.02
     lora_rank: int = 0          # draft-pathway LoRA on the O projection (0: none)
     lora_alpha: float = 0.0
+    norm_gain_std: float = 0.1  # RMSNorm gains are bf16(1 + norm_gain_std * z), one draw per vector
 
     @property
     def mask_token_id(self) -> int:
@@ -110,12 +113,12 @@ def layer_weights(shape: ModelShape, seed: int, layer: int) -> dict:
     not the identity a fresh LoRA would be)."""
     h, s, p = shape.hidden, shape.init_std, "layer%d." % layer
     w = {
-        "attn_norm": bf16_ones(h),
+        "attn_norm": gain_bf16(seed, p + "attn_norm", h, shape.norm_gain_std),
         "wq": normal_bf16(seed, p + "wq", (shape.q_dim, h), s),
         "wk": normal_bf16(seed, p + "wk", (shape.kv_dim, h), s),
         "wv": normal_bf16(seed, p + "wv", (shape.kv_dim, h), s),
         "wo": normal_bf16(seed, p + "wo", (h, shape.q_dim), s),
-        "ffn_norm": bf16_ones(h),
+        "ffn_norm": gain_bf16(seed, p + "ffn_norm", h, shape.norm_gain_std),
         "w_gate": normal_bf16(seed, p + "w_gate", (shape.ffn, h), s),
         "w_up": normal_bf16(seed, p + "w_up", (shape.ffn, h), s),
         "w_down": normal_bf16(seed, p + "w_down", (h, shape.ffn), s),
@@ -140,8 +143,8 @@ def lm_head_weights(shape: ModelShape, seed: int) -> np.ndarray:
     return normal_bf16(seed, "lm_head", (shape.vocab, shape.hidden), shape.init_std)
 
 
-def final_norm_weights(shape: ModelShape) -> np.ndarray:
-    return bf16_ones(shape.hidden)
+def final_norm_weights(shape: ModelShape, seed: int) -> np.ndarray:
+    return gain_bf16(seed, "final_norm", shape.hidden, shape.norm_gain_std)
 
 
 class LazyWeights:
@@ -178,7 +181,7 @@ class LazyWeights:
 
     @property
     def final_norm(self) -> np.ndarray:
-        return final_norm_weights(self.shape)
+        return final_norm_weights(self.shape, self.seed)
 
 
 # ----------------------------------------------------------------------------- K/V and tokens

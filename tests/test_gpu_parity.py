@@ -168,6 +168,23 @@ def test_tiny_block_pass(R, tiny, mode, bidir_from):
     assert int(t["cache"].lengths.cpu()[0]) == 128
 
 
+@pytest.mark.parametrize("kind", ["swap0", "final<-attn1"])
+def test_tiny_misplaced_gain_fails_parity(R, tiny, kind):
+    """Negative control of the gain path: the device pass of a model whose RMSNorm gains were moved
+    (layer 0's attention and FFN gains swapped; layer 1's attention gain at the final norm) is far
+    outside the tolerance against the oracle of the true model, while the true model passes."""
+    from test_oracle_pins import _GainSwap
+    t = tiny
+    bad = R.DeviceModel(t["shape"], _GainSwap(t["src"], kind))
+    ref, _, _ = O.block_forward(t["w"], t["okv"], t["block"], O.VERIFY)
+    ws = R.Workspace(bad, 1, 8, 256)
+    logits, _ = R.block_forward(bad, t["cache"], ws, torch.from_numpy(t["block"]).cuda(), R.VERIFY)
+    e = rel_err(logits.cpu().numpy(), ref)
+    log("tiny with gains moved (%s) against the true oracle: rel err %.3e" % (kind, e))
+    assert e > 5 * TOL
+    bad.close()
+
+
 def test_tiny_self_speculation_loop(R, tiny):
     """Three paper-loop steps (draft -> verify -> accept -> commit) on both sides from the same prefix."""
     t = tiny
@@ -263,6 +280,39 @@ def test_tiny_decode_steps_equal_single_calls(R, tiny):
     assert R.read_device_status(wa) == 0
 
 
+def test_tiny_decode_steps_against_the_oracle(R, tiny):
+    """nld_decode_steps at k = 8 for 3 steps (drafts kept on the device) against three oracle
+    self-speculation steps: accept lengths, committed tokens, the anchor left in place, the lengths and
+    every layer's committed K/V rows."""
+    t = tiny
+    k, n = 8, 3
+    okv = t["okv"].copy()
+    anchor = synth_tokens(t["shape"], 0, "tiny.anchor", (1,))
+    a_o, refs = anchor.copy(), []
+    for _ in range(n):
+        ref = O.self_spec_step(t["w"], okv, a_o, k)
+        refs.append(ref)
+        a_o = ref["next_anchor"]
+    cache = _tiny_cache_copy(R, t)
+    ws = R.Workspace(t["model"], 1, k, 256)
+    a_g = torch.from_numpy(anchor.copy()).cuda()
+    outs = R.decode_steps(t["model"], cache, ws, a_g, k, n)
+    acc, com = outs["accept_len"].cpu().numpy(), outs["committed"].cpu().numpy()
+    for s, ref in enumerate(refs):
+        L = int(ref["L"][0])
+        assert acc[s, 0] == L, "step %d" % s
+        assert com[s, 0].tolist() == ref["committed"][0] + [-1] * (k - L - 1), "step %d" % s
+    assert int(a_g.cpu()[0]) == int(a_o[0])
+    end = int(okv.lengths[0])
+    assert int(cache.lengths.cpu()[0]) == end
+    for l in range(t["shape"].n_layers):
+        kg, vg = cache.read_kv(l, 0, end)
+        assert rel_err(O.bf16_bits_to_float(kg), okv.k[l][:, :, :end]) < TOL
+        assert rel_err(O.bf16_bits_to_float(vg), okv.v[l][:, :, :end]) < TOL
+    assert R.read_device_status(ws) == 0
+    log("tiny decode loop: accept lengths %s" % acc[:, 0].tolist())
+
+
 def test_tiny_decode_steps_ar_mode(R, tiny):
     """With k = 1 the loop is AR decoding: the committed tokens are the oracle's greedy continuation."""
     t = tiny
@@ -298,14 +348,39 @@ def test_draft_with_bidir_from_k_is_the_verify_pass(R, tiny):
 
 
 def test_capacity_error_is_reported_not_written(R, tiny):
-    """A block that would run past max_len sets the capacity bit; no row beyond the cache is written."""
+    """A block that would run past max_len sets the capacity bit; no row beyond the cache is written.
+    A commit that would pass max_len stops the length at max_len: with drafts planted to be accepted in
+    full (L = 7 from length 124 in a cache of 128 rows) the length ends at 128, the capacity bit is set,
+    and cache rows 124..127 hold the verify pass's K/V, which equal the oracle's."""
     t = tiny
+    k = 8
     cache = R.DeviceCache(t["shape"], 1, 128)
     cache.set_lengths([124])
-    ws = R.Workspace(t["model"], 1, 8, 128)
+    ws = R.Workspace(t["model"], 1, k, 128)
     R.block_forward(t["model"], cache, ws, torch.from_numpy(t["block"]).cuda(), R.VERIFY, want_logits=False)
     assert R.read_device_status(ws) & 0x2
     assert R.read_device_status(ws) == 0        # reading clears the sticky bits
+
+    okv = t["okv"].copy()
+    okv.lengths[:] = 124
+    anchor = synth_tokens(t["shape"], 0, "tiny.cap.anchor", (1,))
+    tok, greedy = anchor.copy(), []
+    for _ in range(k):
+        tok, _ = O.ar_step(t["w"], okv, tok)
+        greedy.append(int(tok[0]))
+    cache.k[:, :, :, :128].copy_(t["cache"].k[:, :, :, :128])
+    cache.v.copy_(t["cache"].v[:, :, :, :2])
+    cache.set_lengths([124])
+    drafts = np.array([greedy[:k - 1]], dtype=np.int32)
+    out = R.verify_accept(t["model"], cache, ws, torch.from_numpy(anchor).cuda(), torch.from_numpy(drafts).cuda(), k)
+    assert int(out["accept_len"].cpu()[0]) == k - 1
+    assert out["committed"][0].cpu().tolist() == greedy
+    assert int(cache.lengths.cpu()[0]) == 128
+    assert R.read_device_status(ws) & 0x2
+    for l in range(t["shape"].n_layers):
+        kg, vg = cache.read_kv(l, 0, 128)
+        assert rel_err(O.bf16_bits_to_float(kg), okv.k[l][:, :, :128]) < TOL
+        assert rel_err(O.bf16_bits_to_float(vg), okv.v[l][:, :, :128]) < TOL
 
 
 def test_bad_token_is_reported(R, tiny):

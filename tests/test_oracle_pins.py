@@ -281,6 +281,42 @@ def test_block_pass_matches_torch_library_decoder(mini, mode):
     np.testing.assert_allclose(logits, ref[:, 13:], rtol=1e-9, atol=1e-11)
 
 
+class _GainSwap:
+    """Weights of `src` with RMSNorm gain vectors moved: 'swap<l>' exchanges layer l's attention and FFN
+    gains, 'final<-attn1' puts layer 1's attention gain at the final norm, 'attn1<-attn0' repeats layer
+    0's attention gain in layer 1."""
+
+    def __init__(self, src, kind):
+        self.src, self.kind = src, kind
+        self.embed, self.lm_head = src.embed, src.lm_head
+        self.final_norm = src.layer(1)["attn_norm"] if kind == "final<-attn1" else src.final_norm
+
+    def layer(self, l):
+        d = dict(self.src.layer(l))
+        if self.kind == "swap%d" % l:
+            d["attn_norm"], d["ffn_norm"] = d["ffn_norm"], d["attn_norm"]
+        if self.kind == "attn1<-attn0" and l == 1:
+            d["attn_norm"] = self.src.layer(0)["attn_norm"]
+        return d
+
+
+@pytest.mark.parametrize("kind", ["swap0", "swap1", "final<-attn1", "attn1<-attn0"])
+def test_misplaced_gain_moves_logits_beyond_the_tolerance(kind):
+    """The workloads draw every RMSNorm gain vector separately (bf16(1 + 0.1 z)), so a gain used at the
+    wrong place changes the tiny workload's logits by more than five times the 2e-2 parity tolerance:
+    a GPU path with such a mistake cannot pass the parity tests."""
+    src = LazyWeights(SHAPE_TINY, 0)
+    prefix = synth_tokens(SHAPE_TINY, 0, "tiny.prefix", (1, 128))
+    block = synth_tokens(SHAPE_TINY, 0, "tiny.block", (1, 8))
+    outs = []
+    for s in (src, _GainSwap(src, kind)):
+        w = O.OracleWeights(SHAPE_TINY, s, np.float64)
+        kv = O.OracleKV(SHAPE_TINY, 1, 256, np.float64)
+        O.prefill(w, kv, prefix)
+        outs.append(O.block_forward(w, kv, block, O.VERIFY)[0])
+    assert rel(outs[1], outs[0]) > 5 * 2e-2
+
+
 def test_fp32_oracle_close_to_fp64():
     """P13: on the tiny workload the float32 oracle is within 1e-4 (normwise) of the float64 one."""
     src = LazyWeights(SHAPE_TINY, 0)

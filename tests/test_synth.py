@@ -54,3 +54,19 @@ def test_workload_weight_bytes():
     assert SHAPE_14B.weight_bytes() == 27979939840
     r = WORKLOADS["8b_batch32"].prefix_lengths()
     assert len(r) == 32 and r.min() >= 512 and r.max() <= 8192
+
+
+def test_gain_vectors():
+    """RMSNorm gains bf16(1 + std z): float32 RNE to bf16 of the stream's normals, one stream per name,
+    exact ones at std 0."""
+    g = synth.gain_bf16(2, "layer3.ffn_norm", 4096, 0.1)
+    z = synth.normal_f64(2, "layer3.ffn_norm", (4096,))
+    ref = np.array([synth.f32_to_bf16(float(np.float32(1.0 + 0.1 * v))) for v in z[:512]], dtype=np.uint16)
+    assert np.array_equal(g[:512], ref)
+    f = (g.astype(np.uint32) << 16).view(np.float32)
+    assert abs(f.mean() - 1.0) < 0.01 and abs(f.std() - 0.1) < 0.01
+    assert not np.array_equal(g, synth.gain_bf16(2, "layer3.attn_norm", 4096, 0.1))
+    assert np.array_equal(synth.gain_bf16(2, "x", 7, 0.0), synth.bf16_ones(7))
+    # the array rounding agrees with the scalar one on ties and near-ties
+    x = np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -2.0, 0.5 + 2.0 ** -10, 3.1415927], dtype=np.float32)
+    assert synth.f32_array_to_bf16(x).tolist() == [synth.f32_to_bf16(float(v)) for v in x]
