@@ -362,6 +362,27 @@ nld_status nld_trace_read(float* ms, int32_t* counts, int32_t n);
  * (host pointer) and clears it.  Returns NLD_ERR_DEVICE if any bit was set. */
 nld_status nld_read_device_status(void* workspace, uint32_t* host_bits, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the verify
+ * + acceptance step of nld_verify_accept with no workspace argument.  Its
+ * scratch is a static device array of NLD_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends; the call
+ * itself allocates and frees nothing.  Arguments and results are those of
+ * nld_verify_accept (same kernels, same launch plan).  device_status
+ * (optional device uint32) receives this call's device status bits
+ * (NLD_DEV_*); the scratch's own status word is cleared at the start of every
+ * call.  All calls on one GPU share that GPU's scratch array, which keeps the
+ * last call's contents: calls that overlap on one GPU (several streams or
+ * threads) race and must be serialized by the caller.
+ * Errors as nld_verify_accept; NLD_ERR_CAPACITY when the scratch this batch,
+ * k and max_len need (nld_workspace_bytes) exceeds NLD_NOALLOC_SCRATCH_BYTES
+ * (it holds batch 1 at k <= 16 for the 8B and 14B shapes). */
+#define NLD_NOALLOC_SCRATCH_BYTES (64u << 20)
+nld_status nld_verify_accept_noalloc(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor,
+                                     const int32_t* draft, int32_t batch, int32_t k, int32_t* accept_len,
+                                     int32_t* committed, int32_t* next_anchor, float* logits,
+                                     uint32_t* device_status, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -34,8 +34,10 @@ EXPORTED = [
     "nld_block_forward", "nld_draft", "nld_verify_accept", "nld_accept_workspace_bytes",
     "nld_accept_from_logits", "nld_denoise_step", "nld_refresh_block", "nld_commit_from_logits",
     "nld_decode_steps", "nld_choose_block", "nld_quad_workspace_bytes", "nld_quad_step",
-    "nld_read_device_status", "nld_trace_enable", "nld_trace_read",
+    "nld_read_device_status", "nld_trace_enable", "nld_trace_read", "nld_verify_accept_noalloc",
 ]
+
+NLD_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 TRACE_CLASSES = ["embed", "qkv", "attention", "o_proj", "gate_up", "down", "lm_head", "argmax"]
 
@@ -139,6 +141,9 @@ def load():
     L.nld_trace_enable.argtypes = [c_i32]
     L.nld_trace_read.restype = c_i32
     L.nld_trace_read.argtypes = [P(c_f32), P(c_i32), c_i32]
+    L.nld_verify_accept_noalloc.restype = c_i32
+    L.nld_verify_accept_noalloc.argtypes = [c_vp, P(KVCache), c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                            c_vp]
     _lib = L
     return L
 

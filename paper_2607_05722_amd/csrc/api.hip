@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 using namespace nld;
@@ -1122,6 +1123,82 @@ nld_status nld_read_device_status(void* workspace, uint32_t* host_bits, void* st
     HIP_TRY(launch_fill_zero(workspace, 4, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (*host_bits) return fail(NLD_ERR_DEVICE, "device status bits 0x%x", *host_bits);
+    return NLD_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- allocation-free verify
+// The scratch of nld_verify_accept_noalloc: one copy per device, loaded with the code object.  In host
+// code `scratch` is a stand-in symbol, not a device address; the address each device's copy has comes
+// from hipGetSymbolAddress (with that device current) and is kept per device.  Only that address is
+// ever passed to a kernel or a fill.
+static __device__ __align__(256) unsigned char scratch[NLD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// This device's scratch address; on the device's first call the whole array is zeroed (a fill kernel on
+// `s`), which is the state nld_workspace_init gives a workspace.
+nld_status scratch_of_current_device(hipStream_t s, void** out) {
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= MAX_DEVICES) return fail(NLD_ERR_UNSUPPORTED, "device ordinal %d outside [0, %d)", dev, MAX_DEVICES);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(NLD_ERR_HIP, "hipGetSymbolAddress gave no address for the scratch array");
+        HIP_TRY(launch_fill_zero(p, NLD_NOALLOC_SCRATCH_BYTES, s));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return NLD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nld_status nld_verify_accept_noalloc(const nld_model* m, const nld_kv_cache* kv, const int32_t* anchor,
+                                     const int32_t* draft, int32_t batch, int32_t k, int32_t* accept_len,
+                                     int32_t* committed, int32_t* next_anchor, float* logits,
+                                     uint32_t* device_status, void* stream) {
+    // host checks first, with a non-null stand-in workspace of the maximal size: the layout of this call
+    // must fit the scratch array before anything touches the device
+    Layout L;
+    nld_status st = validate_call(m, kv, batch, k, (void*)&g_scratch_mu, NLD_NOALLOC_SCRATCH_BYTES, &L);
+    if (st == NLD_ERR_CAPACITY)
+        return fail(NLD_ERR_CAPACITY, "this batch (%d), k (%d) and max_len (%d) need %zu bytes of scratch; the "
+                    "allocation-free entry point holds at most %u", batch, k, kv->max_len, L.total,
+                    (unsigned)NLD_NOALLOC_SCRATCH_BYTES);
+    if (st != NLD_OK) return st;
+    if (!anchor || !accept_len || !committed || !next_anchor)
+        return fail(NLD_ERR_INVALID_ARG, "anchor, accept_len, committed or next_anchor is NULL");
+    if (k > 1 && !draft) return fail(NLD_ERR_INVALID_ARG, "draft is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    st = scratch_of_current_device(s, &ws);
+    if (st != NLD_OK) return st;
+    uint32_t* status = at<uint32_t>(ws, L.status);
+    HIP_TRY(launch_fill_zero(status, 4, s));
+    PassIO io{};
+    io.source = SRC_VERIFY;
+    io.anchor = anchor;
+    io.draft_in = draft;
+    io.mode = NLD_MODE_VERIFY;
+    io.logits = logits;
+    io.finish = FINISH_ACCEPT;
+    io.accept_len = accept_len;
+    io.committed = committed;
+    io.next_anchor = next_anchor;
+    io.advance_lengths = true;
+    st = run_pass(m, kv, batch, k, io, ws, L, s);
+    if (st != NLD_OK) return st;
+    if (device_status) HIP_TRY(launch_copy_u32(status, device_status, s));
     return NLD_OK;
 }
 

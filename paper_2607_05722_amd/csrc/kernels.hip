@@ -2284,4 +2284,13 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
     return hipGetLastError();
 }
 
+__global__ void copy_u32_kernel(const uint32_t* src, uint32_t* dst) {
+    if (threadIdx.x == 0) *dst = *src;
+}
+
+hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, hipStream_t s) {
+    launch(copy_u32_kernel, dim3(1), dim3(64), s, src, dst);
+    return hipGetLastError();
+}
+
 }  // namespace nld

@@ -261,6 +261,7 @@ bool trace_launch_events(hipEvent_t* start, hipEvent_t* stop);
 // ---------------------------------------------------------------- launchers (kernels.hip)
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, hipStream_t s);   // *dst = *src (one word)
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 // Normed multi-tile GEMM (M <= 16).  ks = k-steps per wavefront (ksteps = ks * waves); grid = workgroups.
 bool gemm_norm_supported(int ks);

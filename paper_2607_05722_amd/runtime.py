@@ -14,7 +14,7 @@ import torch
 from . import _lib as C
 
 __all__ = ["DeviceModel", "DeviceCache", "Workspace", "block_forward", "draft", "verify_accept",
-           "accept_from_logits", "denoise_step", "refresh_block", "commit_from_logits", "read_device_status",
+           "accept_from_logits", "verify_accept_noalloc", "denoise_step", "refresh_block", "commit_from_logits", "read_device_status",
            "stream_handle", "VERIFY", "DRAFT"]
 
 VERIFY = C.NLD_MODE_VERIFY
@@ -274,6 +274,26 @@ def verify_accept(model, cache, ws, anchor: torch.Tensor, drafts, k: int, want_l
     C.check(C.load().nld_verify_accept(model.handle, ctypes.byref(cache.struct), _ptr(anchor), _ptr(drafts), batch, k,
                                        _ptr(outs["accept_len"]), _ptr(outs["committed"]), _ptr(outs["next_anchor"]),
                                        _ptr(logits), ws.ptr, ws.nbytes, stream_handle()))
+    outs = dict(outs)
+    outs["logits"] = logits
+    return outs
+
+
+def verify_accept_noalloc(model, cache, anchor: torch.Tensor, drafts, k: int, want_logits=False, outs=None,
+                          device_status=None):
+    """verify_accept without a workspace: the library's static per-device scratch array stands in for it.
+    ``device_status`` (optional int32 device tensor of one element) receives the call's status bits."""
+    batch = anchor.shape[0]
+    dev = model.device
+    if outs is None:
+        outs = {"accept_len": torch.empty(batch, dtype=torch.int32, device=dev),
+                "committed": torch.empty((batch, k), dtype=torch.int32, device=dev),
+                "next_anchor": torch.empty(batch, dtype=torch.int32, device=dev)}
+    logits = torch.empty((batch, k, model.shape.vocab), dtype=torch.float32, device=dev) if want_logits else None
+    C.check(C.load().nld_verify_accept_noalloc(model.handle, ctypes.byref(cache.struct), _ptr(anchor), _ptr(drafts),
+                                               batch, k, _ptr(outs["accept_len"]), _ptr(outs["committed"]),
+                                               _ptr(outs["next_anchor"]), _ptr(logits), _ptr(device_status),
+                                               stream_handle()))
     outs = dict(outs)
     outs["logits"] = logits
     return outs
