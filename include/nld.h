@@ -383,6 +383,16 @@ nld_status nld_verify_accept_noalloc(const nld_model* m, const nld_kv_cache* kv,
                                      int32_t* committed, int32_t* next_anchor, float* logits,
                                      uint32_t* device_status, void* stream);
 
+/* HBM streaming-read probe, a measurement aid (not a step of the method): reads
+ * `bytes` (a multiple of 1024) from device buffer `buf` with `grid` workgroups of
+ * `waves` (1..16) wavefronts, each wavefront load one contiguous 1 KiB block (the
+ * weight streams' pattern) and each lane keeping `depth` (4, 8, 16 or 32) loads
+ * in flight; workgroup b writes a checksum to device word sink[b] (grid words).
+ * Bytes over the time of the launch (events on `stream`) is the read rate this
+ * pattern reaches.  Errors: INVALID_ARG, HIP. */
+nld_status nld_hbm_read_probe(const void* buf, size_t bytes, int32_t grid, int32_t waves, int32_t depth,
+                              uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,6 +35,7 @@ EXPORTED = [
     "nld_accept_from_logits", "nld_denoise_step", "nld_refresh_block", "nld_commit_from_logits",
     "nld_decode_steps", "nld_choose_block", "nld_quad_workspace_bytes", "nld_quad_step",
     "nld_read_device_status", "nld_trace_enable", "nld_trace_read", "nld_verify_accept_noalloc",
+    "nld_hbm_read_probe",
 ]
 
 NLD_NOALLOC_SCRATCH_BYTES = 64 << 20
@@ -141,6 +142,8 @@ def load():
     L.nld_trace_enable.argtypes = [c_i32]
     L.nld_trace_read.restype = c_i32
     L.nld_trace_read.argtypes = [P(c_f32), P(c_i32), c_i32]
+    L.nld_hbm_read_probe.restype = c_i32
+    L.nld_hbm_read_probe.argtypes = [c_vp, c_sz, c_i32, c_i32, c_i32, c_vp, c_vp]
     L.nld_verify_accept_noalloc.restype = c_i32
     L.nld_verify_accept_noalloc.argtypes = [c_vp, P(KVCache), c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                             c_vp]

@@ -72,6 +72,26 @@ int env_int(const char* name, int dflt) {
     return (v && *v) ? atoi(v) : dflt;
 }
 
+// Operand sites carried in plain bf16 instead of split form: NLD_PLAIN_SITES, a comma-separated list
+// of norm, final, q, kv, p, o, act (precision knob; default: none, every site split).
+uint32_t plain_sites() {
+    const char* v = getenv("NLD_PLAIN_SITES");
+    if (!v || !*v) return 0u;
+    static const struct { const char* name; uint32_t bit; } names[] = {
+        {"norm", SITE_NORM}, {"final", SITE_FINAL}, {"q", SITE_Q}, {"kv", SITE_KV},
+        {"p", SITE_P}, {"o", SITE_O}, {"act", SITE_ACT}};
+    uint32_t m = 0u;
+    for (const auto& n : names) {
+        const size_t len = strlen(n.name);
+        for (const char* c = v; (c = strstr(c, n.name)) != nullptr; c += len) {
+            const bool start = c == v || c[-1] == ',';
+            const bool end = c[len] == '\0' || c[len] == ',';
+            if (start && end) m |= n.bit;
+        }
+    }
+    return m;
+}
+
 }  // namespace
 
 bool nld::trace_launch_events(hipEvent_t* start, hipEvent_t* stop) {
@@ -507,6 +527,8 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
     e.max_len = kv->max_len;
     e.head_dim = c.head_dim;
     e.quad_k = io.quad_k;
+    const uint32_t plain = plain_sites();
+    e.plain = plain & SITE_NORM;
     for (int i = 0; i < c.head_dim / 2; ++i) e.inv_freq[i] = pow((double)c.rope_base, -2.0 * i / (double)c.head_dim);
     {
         TraceScope ts(NLD_TRACE_EMBED, s);
@@ -543,6 +565,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         g.rope = at<float2>(ws, L.rope);
         g.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * l;
         g.status = status;
+        g.plain = plain & (SITE_Q | SITE_KV);
         {
             TraceScope ts(NLD_TRACE_QKV, s);
             HIP_TRY(normed_gemm(EPI_QKV, g, ws, L, s, nullptr));
@@ -574,6 +597,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.items = L.attn_items ? 1 : 0;
         at_.n_seq = batch;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+        at_.plain = plain & (SITE_P | SITE_O);
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);
             HIP_TRY(launch_attention(D, L.attn_kh, L.attn_z, L.units, at_, s));
@@ -612,6 +636,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         go.xg_out = at<uint16_t>(ws, L.xg);
         go.gain_next = (const uint16_t*)W.ffn_norm;
         go.part_ss_out = at<float>(ws, L.part_ss);
+        go.plain = plain & SITE_NORM;
         {
             TraceScope ts(NLD_TRACE_O_PROJ, s);
             HIP_TRY(resid_gemm(SK_O, go, ws, L, s));
@@ -627,6 +652,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gu.act = at<uint16_t>(ws, L.act);
         gu.ffn = c.ffn;
         gu.tile_ctr = at<unsigned>(ws, L.tile_ctr) + 2 * l + 1;
+        gu.plain = plain & SITE_ACT;
         {
             TraceScope ts(NLD_TRACE_GATE_UP, s);
             HIP_TRY(normed_gemm(EPI_SWIGLU, gu, ws, L, s, nullptr));
@@ -643,6 +669,7 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         gd.xg_out = at<uint16_t>(ws, L.xg);
         gd.gain_next = (const uint16_t*)(l + 1 < c.n_layers ? mdl->layers[l + 1].attn_norm : mdl->w.final_norm);
         gd.part_ss_out = at<float>(ws, L.part_ss);
+        gd.plain = plain & (l + 1 < c.n_layers ? SITE_NORM : SITE_FINAL);
         {
             TraceScope ts(NLD_TRACE_DOWN, s);
             HIP_TRY(resid_gemm(SK_DOWN, gd, ws, L, s));

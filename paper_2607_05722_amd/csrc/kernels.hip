@@ -108,7 +108,7 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, float y, int m, int t
     if (kind == 0) {
         const int G = nq / nkv;
         const int row = (hh % G) * a.k_blk + jb;
-        store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out);
+        store_split(a.q_out, q_index(b * nkv + hh / G, row, dim, a.q_row_tiles, D), out, a.plain & SITE_Q);
         return;
     }
     // K/V: split into the block buffer (what this pass's attention over the block's
@@ -116,7 +116,7 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, float y, int m, int t
     const int kvh = hh - nq - (kind == 2 ? nkv : 0);
     const size_t unit = (size_t)b * nkv + kvh;
     const uint16_t ob = (uint16_t)f32_to_bf16(out);
-    const uint16_t lo = (uint16_t)f32_to_bf16(out - bf16_to_f32(ob));
+    const uint16_t lo = (a.plain & SITE_KV) ? (uint16_t)0 : (uint16_t)f32_to_bf16(out - bf16_to_f32(ob));
     if (kind == 1) {
         a.blk_k[(unit * 2 * 64 + jb) * D + dim] = ob;
         a.blk_k[((unit * 2 + 1) * 64 + jb) * D + dim] = lo;
@@ -137,7 +137,7 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, float y, int m, in
     const float partner = __shfl_xor(y, 8);   // lanes r < 8 hold gate columns, r^8 the matching up columns
     if (m < a.M && r < 8 && col < a.ffn) {
         const float act = y / (1.0f + expf(-y)) * partner;
-        store_split(a.act, split_index(m, col, (a.ffn + 31) / 32), act);
+        store_split(a.act, split_index(m, col, (a.ffn + 31) / 32), act, a.plain & SITE_ACT);
     }
 }
 
@@ -190,7 +190,7 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, float v, int m, int
     const float xn = xres + v;
     if (ok) {
         a.x[(size_t)m * N + n] = xn;
-        store_split(a.xg_out, split_index(m, n, N / 32), xn * gn);
+        store_split(a.xg_out, split_index(m, n, N / 32), xn * gn, a.plain & (SITE_NORM | SITE_FINAL));
     }
     float sq = ok ? xn * xn : 0.f;
     sq += __shfl_xor(sq, 1);
@@ -1716,7 +1716,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
             const int ks = (TPW / 2) * kh + kk;          // 32-key PV step within the stage
             // slot jj of lane group g <-> key kb + 32ks + 8g + jj
             uint4 pop, pol;                               // P^T as split operands
-            split8(p + 8 * kk, pop, pol);
+            split8(p + 8 * kk, pop, pol, a.plain & SITE_P);
             if (m_ref == -INFINITY) pop = pol = zero4;
             const int key0 = kb + 32 * ks + 8 * g;
             const bool vmask = edge && (key0 + 8 > kend);  // V rows past the valid keys may hold anything
@@ -1893,7 +1893,8 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
         for (; sp < ns; ++sp) num += wsh[sp] * a.part_o[(ubase + (size_t)pidx(sp) * a.rows_pad) * D + d];
     }
     const int hl = rw / k, j = rw % k;
-    store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den);
+    store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den,
+                a.plain & SITE_O);
 }
 
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
@@ -1970,7 +1971,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
             *(float4*)(a.x + row + col) = float4{xv[0], xv[1], xv[2], xv[3]};
             *(float4*)(a.x + row + col + 4) = float4{xv[4], xv[5], xv[6], xv[7]};
             uint4 hi, lo;
-            split8(xgv, hi, lo);
+            split8(xgv, hi, lo, a.plain & SITE_NORM);
             const size_t xi = split_index(m, col, a.hidden / 32);
             *(uint4*)(a.xg + xi) = hi;
             *(uint4*)(a.xg + xi + SPLIT_LO) = lo;

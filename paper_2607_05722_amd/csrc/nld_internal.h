@@ -67,14 +67,15 @@ __host__ __device__ __forceinline__ size_t split_index(int m, int k, int ksteps)
 }
 constexpr int SPLIT_LO = 512;   // element offset of a lo value from its hi value
 
-__device__ __forceinline__ void store_split(uint16_t* p, size_t hi_index, float v) {
+// plain != 0: the operand site is carried in plain bf16 (the lo value is stored as zero)
+__device__ __forceinline__ void store_split(uint16_t* p, size_t hi_index, float v, int plain = 0) {
     const uint32_t h = f32_to_bf16(v);
     p[hi_index] = (uint16_t)h;
-    p[hi_index + SPLIT_LO] = (uint16_t)f32_to_bf16(v - bf16_to_f32(h));
+    p[hi_index + SPLIT_LO] = plain ? (uint16_t)0 : (uint16_t)f32_to_bf16(v - bf16_to_f32(h));
 }
 
-// eight floats -> hi and lo operand quads (element e in bits 16(e%2) of word e/2)
-__device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
+// eight floats -> hi and lo operand quads (element e in bits 16(e%2) of word e/2); plain: lo = 0
+__device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo, int plain = 0) {
     uint32_t h[4], l[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -82,8 +83,20 @@ __device__ __forceinline__ void split8(const float* v, uint4& hi, uint4& lo) {
         l[q] = pack_bf16x2(v[2 * q] - bf16_to_f32(h[q] & 0xFFFFu), v[2 * q + 1] - bf16_to_f32(h[q] >> 16));
     }
     hi = uint4{h[0], h[1], h[2], h[3]};
-    lo = uint4{l[0], l[1], l[2], l[3]};
+    lo = plain ? uint4{0u, 0u, 0u, 0u} : uint4{l[0], l[1], l[2], l[3]};
 }
+
+// Operand sites that may be carried in plain bf16 instead of split (hi + lo) form: a precision
+// knob (NLD_PLAIN_SITES on the host); every site is split by default.
+enum PlainSite : uint32_t {
+    SITE_NORM = 1u,    // RMSNorm operands of the QKV and gate/up projections
+    SITE_FINAL = 2u,   // the final RMSNorm operand (LM head input)
+    SITE_Q = 4u,       // queries
+    SITE_KV = 8u,      // the block's own keys and values (the attention's in-pass copy)
+    SITE_P = 16u,      // attention probabilities
+    SITE_O = 32u,      // attention output (O projection input)
+    SITE_ACT = 64u     // SwiGLU output (down projection input)
+};
 
 // ---------------------------------------------------------------- kernel arguments
 enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3, EPI_SPLIT = 4 };
@@ -147,6 +160,9 @@ struct GemmArgs {
     // ens_logits [batch][2 * quad_k][vocab] when that buffer is given.
     int quad_k;
     float* ens_logits;
+    // PlainSite bits of the split operands this GEMM's epilogue writes (EPI_QKV: SITE_Q and SITE_KV;
+    // EPI_SWIGLU: SITE_ACT; EPI_RESID: SITE_NORM, or SITE_FINAL when gain_next is the final norm's)
+    uint32_t plain;
 };
 
 // Queries are stored per (sequence b, KV head) unit with the unit's rows
@@ -177,6 +193,7 @@ struct AttnArgs {
     // part; items past the total leave at once, and the merge reads only the valid parts.
     int items;
     int n_seq;           // sequences (units / n_kv_heads)
+    uint32_t plain;      // PlainSite bits: SITE_P (probabilities), SITE_O (the merged output)
 };
 
 struct EmbedArgs {
@@ -198,6 +215,7 @@ struct EmbedArgs {
     const int32_t* lengths;
     int max_len, head_dim;
     int quad_k;             // source 3: chain length of the quadratic layout (block row positions follow it)
+    uint32_t plain;         // SITE_NORM: the first layer's RMSNorm operand in plain bf16
     double inv_freq[64];    // base^(-2i/head_dim), computed on the host in fp64
 };
 
