@@ -273,7 +273,7 @@ def cpu_baseline(wl, k, min_seconds=10.0, max_passes=8):
     total = sum(times)
     return {
         "value": round(k * len(times) / total, 4), "unit": "block tokens/s", "cores": int(blas_threads()),
-        "kind": "oracle",
+        "kind": "oracle", "cpu_model": cpu_model_name(), "host_cpus": os.cpu_count(),
         "sample": "fp32 numpy oracle, %d full verify passes (batch 1 of the workload, k=%d, prefix %d, all %d layers "
                   "+ LM head), %.1f s in total" % (len(times), k, P, shape.n_layers, total),
     }
@@ -308,46 +308,140 @@ def measured_traffic(kernel):
         return None
 
 
-def copy_ceiling(gib=2, reps=5):
-    """Practical HBM ceiling: GB/s (bytes read + written) of a plain device-to-device copy of `gib` GiB,
-    alternating between two buffer pairs so that no copy finds its source in the memory-side cache."""
+def hbm_ceiling():
+    """What a plain read stream reaches on this part: the library's streaming probe (one contiguous 1 KiB
+    block per wavefront load, 16 loads in flight per lane) over 2 GiB at several grid shapes, each launch
+    reading a different region of an 8 GiB pool so that none finds its data in the memory-side cache.
+    Also the time of 16, 50 and 200 MiB reads, whose intercept is the fixed cost of one launch."""
     import torch
-    n = gib * (1 << 30) // 4
-    bufs = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(4)]
-    for b in bufs:
-        b.fill_(1.0)
-    bufs[1].copy_(bufs[0])
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(reps):
-        src, dst = (bufs[0], bufs[1]) if i % 2 == 0 else (bufs[2], bufs[3])
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    gbps = 2.0 * n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del bufs
+    from paper_2607_05722_amd import _lib as C
+    lib = C.load()
+    pool_bytes = 8 << 30
+    pool = torch.ones(pool_bytes // 4, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(65536, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+
+    def run(nbytes, grid, waves, depth, reps):
+        offs = [((i * nbytes) % (pool_bytes - nbytes)) // 1024 * 1024 for i in range(reps + 1)]
+        C.check(lib.nld_hbm_read_probe(pool.data_ptr() + offs[0], nbytes, grid, waves, depth, sink.data_ptr(), s))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(reps):
+            C.check(lib.nld_hbm_read_probe(pool.data_ptr() + offs[i + 1], nbytes, grid, waves, depth, sink.data_ptr(),
+                                           s))
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3   # us per launch
+
+    shapes = {}
+    for grid, waves, depth in ((256, 16, 16), (512, 16, 16), (1024, 16, 16), (2048, 16, 16)):
+        us = run(2 << 30, grid, waves, depth, 4)
+        shapes["%dx%dx%d" % (grid, waves, depth)] = round((2 << 30) / (us * 1e-6) / 1e9, 1)
+    sizes = {mib: run(mib << 20, 256, 16, 16, 10) for mib in (16, 50, 200)}
+    slope = (sizes[200] - sizes[50]) / (150 << 20)              # us per byte
+    del pool
     torch.cuda.empty_cache()
-    return round(gbps, 1)
+    best = max(shapes, key=shapes.get)
+    return {"read_GBps": shapes[best], "frac": round(shapes[best] / HBM_PEAK_GBS, 4),
+            "grid_x_waves_x_depth": best, "by_shape_GBps": shapes,
+            "us_per_launch": {"%d MiB" % m: round(v, 2) for m, v in sizes.items()},
+            "fixed_us_per_launch": round(sizes[50] - slope * (50 << 20), 2),
+            "marginal_GBps": round(1e-3 / slope, 1),
+            "note": "nld_hbm_read_probe, launches timed back to back with events (launch gaps included)"}
 
 
-def read_ceiling(gib=4, reps=5):
-    """GB/s of a device-wide sum over `gib` GiB (reads only; torch's reduction kernel)."""
+def verify_pass_timing(R, model, cache, ws, anchor, k, reps):
+    """Mean ms of one verify pass (verify + argmax + acceptance + commit) replayed from a captured graph with
+    the lengths reset first, on drafts from one draft pass."""
     import torch
-    n = gib * (1 << 30) // 4
-    x = torch.ones(n, dtype=torch.float32, device="cuda")
-    x.sum()
+    B, dev = anchor.shape[0], anchor.device
+    a0 = anchor.clone()
+    d = torch.empty((B, k - 1), dtype=torch.int32, device=dev)
+    R.draft(model, cache, ws, a0, k, out=d)
+    len0 = cache.lengths.clone()
+    outs = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+            "committed": torch.empty((B, k), dtype=torch.int32, device=dev),
+            "next_anchor": torch.empty(B, dtype=torch.int32, device=dev)}
+
+    def verify():
+        cache.lengths.copy_(len0)
+        R.verify_accept(model, cache, ws, a0, d, k, outs=outs)
+
+    ms = graph_ms(verify, reps)
+    cache.lengths.copy_(len0)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        x.sum()
-    e1.record()
+    return ms
+
+
+def large_config(R, name, reps=8):
+    """One draft + verify + accept step of a many-row configuration (8b_batch32: 32 ragged sequences of the
+    8B stack, 512 block rows; 14b: 8 sequences of the 14B stack at k = 32, 256 rows), replayed from a captured
+    graph with the lengths reset first: step and verify-pass times, their fractions of the HBM roofline on
+    the pass bytes, the algorithmic MFMA rate, and the per-kernel times of three traced steps.  Weights come
+    from the seeded generator; the K/V caches are filled on the device with seeded N(0, 1) bf16 values
+    (torch's generator: only the timing is measured here; the parity tests use the oracle's inputs)."""
+    import torch
+    from synth.workloads import LazyWeights, WORKLOADS, tokens
+    wl = WORKLOADS[name]
+    shape, k, B = wl.shape, wl.k_values[0], wl.batch
+    plens = wl.prefix_lengths()
+    max_len = int(-(-(int(plens.max()) + 2 * k) // 64) * 64)
+    t0 = time.perf_counter()
+    model = R.DeviceModel(shape, LazyWeights(shape, wl.seed, keep=False))
+    cache = R.DeviceCache(shape, B, max_len)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1000 + wl.seed)
+    for l in range(shape.n_layers):
+        for t in (cache.k[l], cache.v[l]):
+            t.view(torch.bfloat16).copy_(torch.randn(t.shape, generator=gen, device="cuda", dtype=torch.float32))
+    cache.set_lengths(plens)
+    ws = R.Workspace(model, B, k, max_len)
     torch.cuda.synchronize()
-    gbps = n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del x
+    log("%s: model and cache ready in %.1f s" % (name, time.perf_counter() - t0))
+    dev = torch.device("cuda")
+    a0 = torch.from_numpy(tokens(shape, wl.seed, "bench.%s.anchor" % name, (B,))).to(dev)
+    len0 = cache.lengths.clone()
+    i32 = lambda *shp: torch.empty(shp, dtype=torch.int32, device=dev)
+    d, outs = i32(B, k - 1), {"accept_len": i32(B), "committed": i32(B, k), "next_anchor": i32(B)}
+
+    def step():
+        cache.lengths.copy_(len0)
+        R.draft(model, cache, ws, a0, k, out=d)
+        R.verify_accept(model, cache, ws, a0, d, k, outs=outs)
+
+    step_ms = graph_ms(step, reps)
+    verify_ms = verify_pass_timing(R, model, cache, ws, a0, k, reps)
+    kernels = traced_kernels(step, 3)
+    status = R.read_device_status(ws)
+    pb, pf = pass_bytes(shape, B, k, plens), pass_flops(shape, B, k, plens)
+    res = {
+        "workload": "%s: %d layers, hidden %d, %d/%d heads, ffn %d; batch %d, prefix %s, k=%d" % (
+            name, shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.ffn, B,
+            "ragged %d..%d" % wl.ragged if wl.ragged else int(plens[0]), k),
+        "rows_per_pass": B * k,
+        "step_ms": round(step_ms, 3), "verify_pass_ms": round(verify_ms, 3),
+        "block_tokens_per_s": round(2.0 * B * k / (step_ms * 1e-3), 1),
+        "step_hbm_frac": round(2 * pb / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "algorithmic_TFLOPs": round(2 * pf / (step_ms * 1e-3) / 1e12, 1),
+        "mfma_frac_of_bf16_peak": round(2 * pf / (step_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "note": "split activation operands: the issued MFMA work is about twice the algorithmic",
+        "kernels_us": kernels, "device_status": status,
+    }
+    model.close()
+    del model, cache, ws
     torch.cuda.empty_cache()
-    return round(gbps, 1)
+    return res
+
+
+def cpu_model_name():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def layer_microbench(R, reps=20):
@@ -403,6 +497,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the Mode 2 and LoRA timings (counter runs use this: eager launches only)")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the 8b_batch32 and 14b step timings of the extras")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run plain copies of this many MiB (reference dispatches for counter runs)")
     args = ap.parse_args()
@@ -501,6 +597,8 @@ def main():
         C.check(lib.nld_trace_read(ms, cnt, 8))
         lib.nld_trace_enable(0)
 
+        verify_ms = verify_pass_timing(R, model, cache, ws, anchor, k, max(5, steps // 2)) if graph is not None \
+            else None
         m2_ms = lora_ms = quad_ms = layer_ms = k32_ms = None
         if not args.no_extras:
             block_full = torch.from_numpy(tokens(shape, wl.seed, "bench.m2.block", (B, k))).to(dev)
@@ -548,7 +646,10 @@ def main():
                                   shape.head_dim, shape.ffn, shape.vocab, B,
                                   int(plens[0]) if wl.ragged is None else "ragged %d..%d" % wl.ragged, k),
                    "graph": graph is not None, "kv_capacity": max_len},
-        "pass_ms": round(ms_per_step / 2, 4),
+        "verify_pass_ms": round(verify_ms, 4) if verify_ms is not None else None,
+        "verify_pass_block_tokens_per_s": round(B * k / (verify_ms * 1e-3), 1) if verify_ms is not None else None,
+        "verify_pass_hbm_frac": round(pass_bytes(shape, B, k, plens) / (verify_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        if verify_ms is not None else None,
         "step_hbm_GBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
         "step_hbm_frac": round(bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_step": int(bytes_step),
@@ -583,8 +684,8 @@ def main():
                                          / HBM_PEAK_GBS, 4),
         }
     if not args.no_extras:
-        res["hbm_copy_GBps"] = copy_ceiling()   # what a plain copy reaches on this part (read + write)
-        res["hbm_sum_read_GBps"] = read_ceiling()   # and a plain reduction (reads only)
+        res["hbm_stream_ceiling"] = hbm_ceiling()   # what a plain read stream reaches on this part
+        res["step_frac_of_stream_ceiling"] = round(res["step_hbm_GBps"] / res["hbm_stream_ceiling"]["read_GBps"], 4)
         res["layer_microbench"] = layer_ms
     if k32_ms is not None:
         res["block_k32"] = {
@@ -604,9 +705,14 @@ def main():
                                    / HBM_PEAK_GBS, 4),
             "kernels": quad_ms["kernels_us"],
         }
-    if not args.no_cpu_baseline:
+    if not args.no_extras or not args.no_cpu_baseline:
+        model.close()
         del model, cache, ws
         torch.cuda.empty_cache()
+    if not args.no_extras and not args.no_large:
+        with torch.cuda.stream(torch.cuda.Stream()):     # graphs are captured on a non-default stream
+            res["large_configs"] = {name: large_config(R, name) for name in ("8b_batch32", "14b")}
+    if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, k)
     print(json.dumps(res), flush=True)
 
