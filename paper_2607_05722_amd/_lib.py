@@ -80,14 +80,17 @@ def lib_path() -> str:
     return _build.LIB
 
 
-def load():
-    """Load libnld.so (building it first only when it does not exist)."""
+def load(path: str = None):
+    """Load libnld.so (building it first only when it does not exist).  `path` (first call only) loads
+    another build of the same ABI instead, such as the timeline build of timeline.py."""
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_build.LIB):
-        _build.build()
-    L = ctypes.CDLL(_build.LIB)
+    if path is None:
+        path = _build.LIB
+        if not os.path.exists(path):
+            _build.build()
+    L = ctypes.CDLL(path)
     P = ctypes.POINTER
     L.nld_last_error.restype = ctypes.c_char_p
     L.nld_last_error.argtypes = []

@@ -310,8 +310,10 @@ StreamPlan plan_stream(int epi, int M, int n_tiles) {
         p.ct = 2;
         p.nw = 8;
     } else {
+        // O and down on this kernel at up to 16 rows: 16 wavefronts with every load of their 8 k-steps in
+        // flight (O at the 8B shapes: 10.8-11.0 against 11.2 us with 8 wavefronts)
         p.ct = 1;
-        p.nw = 8;
+        p.nw = epi == EPI_RESID && M <= 16 ? env_int("NLD_STREAM_NW_RESID", 16) : 8;
     }
     p.gx = cdiv(n_tiles, p.ct);
     return p;
@@ -455,7 +457,8 @@ hipError_t resid_gemm(int kind, const GemmArgs& g, void* ws, const Layout& L, hi
     if (plan_splitk(kind, EPI_RESID, g, L, &ct, &ksplit))
         return launch_gemm_splitk(EPI_RESID, ct, ksplit, g, at<float>(ws, L.sk_part),
                                   at<unsigned>(ws, L.tile_ctr) + L.sk_ctr0, s);
-    const StreamPlan p = plan_stream(EPI_RESID, g.M, g.n_tiles);
+    StreamPlan p = plan_stream(EPI_RESID, g.M, g.n_tiles);
+    if (g.W2) p.nw = 8;   // the second source's k-steps need the 8-wavefront kernel's registers
     return launch_gemm_stream(EPI_RESID, p.mt, p.ct, p.nw, p.gx, p.gy, g, s);
 }
 

@@ -47,6 +47,22 @@
 
 namespace nld {
 
+// Per-workgroup phase timestamps (a diagnostic build only, -DNLD_TIMELINE; see timeline.py): thread 0
+// of each workgroup records the 100 MHz real-time counter at the phase boundaries of the kernels of
+// one layer pass, class x workgroup x phase.  In the normal build NLD_TS expands to nothing.
+#ifdef NLD_TIMELINE
+__device__ unsigned long long g_timeline[8][8192][8];
+#define NLD_TS(cls, ph)                                                                                   \
+    do {                                                                                                  \
+        if (threadIdx.x == 0)                                                                             \
+            g_timeline[cls][blockIdx.x + blockIdx.y * gridDim.x + blockIdx.z * gridDim.x * gridDim.y][ph] = \
+                __builtin_amdgcn_s_memrealtime();                                                         \
+    } while (0)
+#else
+#define NLD_TS(cls, ph) do { } while (0)
+#endif
+enum TimelineClass { TL_QKV = 0, TL_ATTENTION = 1, TL_COMBINE = 2, TL_GATE_UP = 3, TL_O = 4, TL_DOWN = 5, TL_LM = 6 };
+
 // Every kernel launch goes through here: a plain launch, or, while launch tracing is on,
 // a launch whose start and stop events are recorded on the dispatch itself.
 template <typename... KArgs, typename... Args>
@@ -238,6 +254,8 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
 
     __shared__ int next_s[2];
 
+    constexpr int TLC = EPI == EPI_QKV ? TL_QKV : (EPI == EPI_SWIGLU ? TL_GATE_UP : TL_LM);
+    NLD_TS(TLC, 0);
     const int NW = blockDim.x >> 6;
     if constexpr (EPI == EPI_LMHEAD) {
         if (threadIdx.x < 256) {
@@ -286,6 +304,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
 
     // A tile is finished by FIN wavefronts (wavefront i of the group takes rows 4g + i,
     // 4g + i + FIN, ...); the groups take the tiles in turn.
+    NLD_TS(TLC, 1);   // operand, first tile and row statistics in
     const int FIN = NW < 4 ? NW : 4, groups = NW / FIN;
     for (int it = 0; cur < T; ++it) {
         const int t = cur;
@@ -326,6 +345,7 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
         }
     }
 
+    NLD_TS(TLC, 2);
     if constexpr (EPI == EPI_LMHEAD) {
         // one argmax key per row for this workgroup
         __syncthreads();
@@ -627,10 +647,11 @@ hipError_t launch_gemm_normk(int epi, int grid_x, const GemmArgs& a, float* part
 // projections (residual epilogue) and, for M > 16, for every projection (the
 // per-row RMSNorm scale is then formed in the prologue).
 // =====================================================================================
-template <int MT, int CT, bool SPLIT>
+template <int MT, int CT, bool SPLIT, int NW = 8>
 struct Batch {
     static constexpr int OPS = CT + MT * (SPLIT ? 2 : 1);   // operand quads per k-step
-    static constexpr int U = (OPS <= 3) ? 8 : ((OPS <= 5) ? 4 : 2);
+    // 16 wavefronts (1024 threads, at most 128 registers each): half the batch
+    static constexpr int U = ((OPS <= 3) ? 8 : ((OPS <= 5) ? 4 : 2)) / (NW > 8 ? 2 : 1);
     uint4 w[U][CT];
     uint4 x[U][MT];
     uint4 xl[SPLIT ? U : 1][SPLIT ? MT : 1];
@@ -640,13 +661,14 @@ template <int MT, int CT, int NW, int EPI, bool XK>
 __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
     constexpr bool SPLIT = true;
     constexpr bool NORMED = EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LMHEAD;
-    typedef Batch<MT, CT, SPLIT> B;
+    typedef Batch<MT, CT, SPLIT, NW> B;
     constexpr int U = B::U;
     constexpr int BSTRIDE = SPLIT ? 1024 : 512;   // elements per (row tile, k-step) block
     __shared__ f32x4_t red[NW][MT * CT][64];
     __shared__ unsigned long long key_s[16 * MT];
     __shared__ float2 lse_s[16 * MT][CT];
     __shared__ float inv_s[16 * MT];
+    NLD_TS(TL_O, 0);
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -766,6 +788,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
         compute(b1);
     }
 
+    NLD_TS(TL_O, 1);   // main loop done
     if constexpr (XK) {
 #pragma unroll
         for (int i = 0; i < XS; ++i)
@@ -841,11 +864,18 @@ __global__ void __launch_bounds__(NW * 64) gemm_stream_kernel(GemmArgs a) {
             }
         }
     }
+#ifdef NLD_TIMELINE
+    __syncthreads();
+#endif
+    NLD_TS(TL_O, 2);
 }
 
 template <int EPI, int MT, bool XK>
 static hipError_t launch_stream_ct(int ct, int nw, dim3 grid, const GemmArgs& a, hipStream_t s) {
     if (ct == 1 && nw == 8) launch(gemm_stream_kernel<MT, 1, 8, EPI, XK>, dim3(grid), dim3(512), s, a);
+    else if (ct == 1 && nw == 16 && !XK) {
+        if constexpr (!XK) launch(gemm_stream_kernel<MT, 1, 16, EPI, false>, dim3(grid), dim3(1024), s, a);
+    }
     else if (ct == 2 && nw == 8) launch(gemm_stream_kernel<MT, 2, 8, EPI, XK>, dim3(grid), dim3(512), s, a);
     else if (ct == 4 && nw == 4) launch(gemm_stream_kernel<MT, 4, 4, EPI, XK>, dim3(grid), dim3(256), s, a);
     else if (ct == 1 && nw == 4) launch(gemm_stream_kernel<MT, 1, 4, EPI, XK>, dim3(grid), dim3(256), s, a);
@@ -917,6 +947,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
     __shared__ f32x4_t red[NW][NTL][64];
     __shared__ float inv_s[16 * MT];
     __shared__ int last_s;
+    NLD_TS(TL_DOWN, 0);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -1016,6 +1047,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
             else red[wave][mt * CT + ct][lane] = acc[mt][ct] + accl[mt][ct];
         }
     __syncthreads();
+    NLD_TS(TL_DOWN, 1);   // main loop done
 
     typedef unsigned long long u64;
     // the workgroup's partials of the wavefront's tiles ti = wave, wave + NW, ... (fixed order over
@@ -1051,6 +1083,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
         if (threadIdx.x == 0)
             last_s = __hip_atomic_fetch_add(ctr + cg, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(ksplit - 1);
         __syncthreads();
+        NLD_TS(TL_DOWN, 2);   // partial counted in
         if (!last_s) return;
         if (threadIdx.x == 0) __hip_atomic_exchange(ctr + cg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
@@ -1518,6 +1551,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     // two stage slots, each K tile (KCHUNKS) followed by the V tile (VCHUNKS)
     __shared__ uint4 lds[2 * C::CHUNKS];
 
+    NLD_TS(TL_ATTENTION, 0);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     int split = blockIdx.x, unit = blockIdx.y;
@@ -1645,6 +1679,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const int kbeg = blockpart ? P : split_beg;
     const int kend = blockpart ? P + k : min(kbeg + chunk, P);
     const int nst = blockpart ? 1 : (kend > kbeg ? (kend - kbeg + 63) / 64 : 0);
+    NLD_TS(TL_ATTENTION, 1);   // committed length known
     if (!blockpart) {
         if (nst > 1) s1 = gload(kbeg + 64);
         if (nst > 2) s2 = gload(kbeg + 128);
@@ -1751,6 +1786,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         // two so that no register copy waits on a load still in flight).
         if (nst > 0) lstore(s0, 0);
         __syncthreads();
+        NLD_TS(TL_ATTENTION, 2);   // first stage in LDS
         for (int st = 0; st < nst; st += 2) {
             compute(kbeg + 64 * st, 0, false);
             if (st + 1 < nst) lstore(s1, 1);
@@ -1764,6 +1800,7 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         }
     }
 
+    NLD_TS(TL_ATTENTION, 3);   // stages done
     float l_tot = l_part + __shfl_xor(l_part, 16);
     l_tot += __shfl_xor(l_tot, 32);
     if constexpr (KH == 2) {
@@ -1799,6 +1836,10 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) *(float4*)(po + 16 * dt + 4 * g) = float4{acc[dt][0], acc[dt][1], acc[dt][2], acc[dt][3]};
     if (g == 0) *(float2*)(a.part_ml + pbase * 2) = float2{m_ref, l_tot};
+#ifdef NLD_TIMELINE
+    __syncthreads();
+#endif
+    NLD_TS(TL_ATTENTION, 4);
 }
 
 // Merge of the partials (prefix splits + block part): one workgroup per (unit, query
@@ -1807,6 +1848,7 @@ template <int D>
 __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     __shared__ float wsh[256];
     __shared__ float inv_den;
+    NLD_TS(TL_COMBINE, 0);
     const int unit = blockIdx.x, rw = blockIdx.y, d = threadIdx.x;
     const int nkv = a.n_kv_heads, G = a.n_q_heads / nkv;
     const int b = unit / nkv, kvh = unit % nkv, k = a.k_blk;
@@ -1895,6 +1937,7 @@ __global__ void __launch_bounds__(D) attention_combine_kernel(AttnArgs a) {
     const int hl = rw / k, j = rw % k;
     store_split(a.o, split_index(b * k + j, (kvh * G + hl) * D + d, a.n_q_heads * D / 32), num * inv_den,
                 a.plain & SITE_O);
+    NLD_TS(TL_COMBINE, 1);
 }
 
 hipError_t launch_attention(int head_dim, int kh, int zslices, int units, const AttnArgs& a, hipStream_t s) {
@@ -2295,3 +2338,14 @@ hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, hipStream_t s) {
 }
 
 }  // namespace nld
+
+#ifdef NLD_TIMELINE
+// copies the phase timestamps (8 x 8192 x 8 uint64) to host memory, or clears them (host == NULL)
+extern "C" int nld_timeline_read(void* host, size_t bytes) {
+    if (!host) {
+        static unsigned long long zero[8 * 8192 * 8];
+        return (int)hipMemcpyToSymbol(HIP_SYMBOL(nld::g_timeline), zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+    }
+    return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(nld::g_timeline), bytes, 0, hipMemcpyDeviceToHost);
+}
+#endif

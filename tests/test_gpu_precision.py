@@ -1,12 +1,12 @@
 """Precision budget of the split operands: the error each operand site adds at full depth when it is
 carried in plain bf16 instead of split (hi + lo) form.
 
-The study is opt-in (NLD_PRECISION_STUDY=1; about two minutes of oracle work): it runs the 36-layer
+The study is opt-in (NLD_PRECISION_STUDY=1; about a minute of oracle work; skipped otherwise, the default
+configuration's parity at these sizes being the full-workload tests' business): it runs the 36-layer
 8B draft and verify passes (batch 1, prefix 4096, k = 16) and the 40-layer 14B verify pass (one
 sequence of the batch-8 workload, prefix 16384, k = 32) once per site configuration, each against
 the same oracle passes, and prints one line per configuration (some of them exceed the parity bar:
-that is what the study measures).  The default run checks only the library's default configuration
-against the bar.
+that is what the study measures); the library's default configuration is held to the bar.
 """
 import os
 
@@ -53,12 +53,13 @@ def _setup(R, name, seqs):
 
 
 def _study(R, monkeypatch, name, seqs, modes):
+    if not os.environ.get("NLD_PRECISION_STUDY"):
+        pytest.skip("opt-in study (NLD_PRECISION_STUDY=1)")
     wl, shape, k, model, cache, okv, w = _setup(R, name, seqs)
     blk = synth_tokens(shape, wl.seed, "precision.%s.block" % name, (len(seqs), k))
     refs = {m: O.block_forward(w, okv, blk, m)[0] for m in modes}
     ws = R.Workspace(model, len(seqs), k, cache.max_len)
-    configs = CONFIGS if os.environ.get("NLD_PRECISION_STUDY") else [""]
-    for cfg in configs:
+    for cfg in CONFIGS:
         monkeypatch.setenv("NLD_PLAIN_SITES", cfg)
         errs = []
         for m in modes:
