@@ -101,10 +101,11 @@ def test_8b_full_self_speculation_step(R):
 
 def test_8b_batch32_ragged_verify(R):
     """36-layer 8B, batch 32 with ragged prefixes in [512, 8192], k=16, verify mask: sequences with the
-    shortest and the longest prefix are recomputed by the oracle."""
+    shortest, the longest and a middle prefix are recomputed by the oracle."""
     wl = WORKLOADS["8b_batch32"]
     plens = wl.prefix_lengths()
-    seqs = [int(np.argmin(plens)), int(np.argmax(plens))]
+    order = np.argsort(plens, kind="stable")
+    seqs = [int(order[0]), int(order[-1]), int(order[len(order) // 2])]
     wl, shape, k, B, plens, max_len, model, cache, okv, w = _setup(R, "8b_batch32", seqs)
     blk = synth_tokens(shape, wl.seed, "test.8b_batch32.block", (B, k))
     ws = R.Workspace(model, B, k, max_len)

@@ -13,6 +13,7 @@ import pytest
 import torch
 import torch.nn.functional as F
 
+import synth
 from oracle import nld_oracle as O
 from synth.workloads import LazyWeights, ModelShape, SHAPE_TINY, tokens as synth_tokens
 
@@ -589,6 +590,42 @@ def test_lora_draft_equals_full_recompute(lora_mini):
     seq = np.concatenate([prefix, block], axis=1)
     full = O.full_forward(w, seq, O.sequence_visibility(P, k, O.DRAFT), lora_rows=np.arange(P + k) >= P)
     np.testing.assert_allclose(got, full[:, P:], rtol=1e-10, atol=1e-12)
+
+
+class _LowRankO(O.OracleWeights):
+    """MINI_LORA with a rank-r output projection W_o = B0 A0 in every layer and, with `cancel`, the adapter
+    A = A0, B = -(r / alpha) B0; without it, no adapter and W_o = 0 (float64)."""
+
+    def __init__(self, cancel):
+        super().__init__(MINI_LORA, LazyWeights(MINI_LORA, 11), np.float64)
+        self.cancel = cancel
+
+    def layer(self, l):
+        w = super().layer(l)
+        s, r = self.shape, self.shape.lora_rank
+        a0 = 0.02 * synth.normal_f64(11, "pin.lowrank.a%d" % l, (r, s.q_dim))
+        b0 = 0.35 * synth.normal_f64(11, "pin.lowrank.b%d" % l, (s.hidden, r))
+        del w["lora_a"], w["lora_b"]
+        if self.cancel:
+            w["wo"] = b0 @ a0
+            w["lora_a"], w["lora_b"] = a0, -(r / s.lora_alpha) * b0
+        else:
+            w["wo"] = np.zeros_like(w["wo"])
+        return w
+
+
+def test_lora_scale_cancels_a_low_rank_output_projection(lora_mini):
+    """Pins the adapter's output scale alpha/r (Sec. 3.3: rank 128 with alpha 512) by a closed form rather
+    than by restating it: with a rank-r O projection W_o = B0 A0 and the adapter A = A0, B = -(r/alpha) B0,
+    the draft pathway's projection W_o + scale * B A vanishes exactly when scale = alpha/r, so the draft
+    pass equals that of the model with W_o = 0; the verify pass keeps W_o and differs from it."""
+    _, base, prefix, block = lora_mini
+    kv = prefilled(base, prefix)
+    cancel, zero = _LowRankO(True), _LowRankO(False)
+    d_cancel = O.block_forward(cancel, kv, block, O.DRAFT)[0]
+    d_zero = O.block_forward(zero, kv, block, O.DRAFT)[0]
+    np.testing.assert_allclose(d_cancel, d_zero, rtol=1e-9, atol=1e-11)
+    assert rel(O.block_forward(cancel, kv, block, O.VERIFY)[0], O.block_forward(zero, kv, block, O.VERIFY)[0]) > 1e-3
 
 
 # ----------------------------------------------------------------------------- quadratic self-speculation
