@@ -419,6 +419,8 @@ __global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part
     __shared__ unsigned long long key_s[NW][16];
     __shared__ float2 lse_s[NW][16];
     typedef unsigned long long u64;
+    constexpr int TLC = EPI == EPI_QKV ? TL_QKV : (EPI == EPI_SWIGLU ? TL_GATE_UP : TL_LM);
+    NLD_TS(TLC, 0);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -546,6 +548,7 @@ __global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part
     for (int p = 0; p < PF - 1; ++p)
         if (j0 + p < nt) tile(j0 + p, p, wb[p]);
 
+    NLD_TS(TLC, 1);   // main loop done
     {   // the tiles this workgroup completes (with a single slice: all of its own)
         // every lane's partial stores are acknowledged before the workgroup counts itself in
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -586,6 +589,7 @@ __global__ void __launch_bounds__(512) gemm_normk_kernel(GemmArgs a, float* part
             if (c2 < nfin) epilogue(vb, tb, mt);
         }
     }
+    NLD_TS(TLC, 2);   // completed tiles finished
 
     if constexpr (EPI == EPI_LMHEAD) {
         // one argmax key (and softmax statistics) per row for this workgroup
@@ -947,7 +951,11 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
     __shared__ f32x4_t red[NW][NTL][64];
     __shared__ float inv_s[16 * MT];
     __shared__ int last_s;
-    NLD_TS(TL_DOWN, 0);
+    // timeline class: a residual projection whose reduction is longer than its output is the down
+    // projection, otherwise the O projection
+    const int TLC = EPI == EPI_QKV ? TL_QKV : (EPI == EPI_SWIGLU ? TL_GATE_UP : (a.K > a.n_tiles * 16 ? TL_DOWN : TL_O));
+    (void)TLC;
+    NLD_TS(TLC, 0);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
@@ -1047,7 +1055,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
             else red[wave][mt * CT + ct][lane] = acc[mt][ct] + accl[mt][ct];
         }
     __syncthreads();
-    NLD_TS(TL_DOWN, 1);   // main loop done
+    NLD_TS(TLC, 1);   // main loop done
 
     typedef unsigned long long u64;
     // the workgroup's partials of the wavefront's tiles ti = wave, wave + NW, ... (fixed order over
@@ -1083,7 +1091,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_splitk_kernel(GemmArgs a, float*
         if (threadIdx.x == 0)
             last_s = __hip_atomic_fetch_add(ctr + cg, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(ksplit - 1);
         __syncthreads();
-        NLD_TS(TL_DOWN, 2);   // partial counted in
+        NLD_TS(TLC, 2);   // partial counted in
         if (!last_s) return;
         if (threadIdx.x == 0) __hip_atomic_exchange(ctr + cg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll

@@ -11,6 +11,7 @@ QKV GEMM.  The passes are eager launches (no graph), so the gaps between kernels
 overhead of the host.  Phases:
 
     qkv, gate_up   0-1 operand, first weight tile and row statistics in; 1-2 tiles and epilogues
+                   (17..64 rows: 0-1 main loop; 1-2 completed tiles reduced and finished)
     attention      0-1 committed length known; 1-2 first key stage in LDS; 2-3 stages; 3-4 partials out
     combine        0-1 the whole merge
     o_proj         0-1 main loop; 1-2 reduction and residual epilogue
