@@ -601,6 +601,11 @@ nld_status run_pass(const nld_model* mdl, const nld_kv_cache* kv, int batch, int
         at_.n_seq = batch;
         at_.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
         at_.plain = plain & (SITE_P | SITE_O);
+        // Prefix stages 1 and 2 are requested once stage 0 is in LDS: requested with it, the three
+        // stages of every workgroup arrive interleaved and stage 0 comes late (8B shapes, k = 16:
+        // 16.55 against 17.43 us per attention and merge).  NLD_ATTN_LATE = 0 / 1: all at once /
+        // stage 2 only.
+        at_.late = env_int("NLD_ATTN_LATE", 2);
         {
             TraceScope ts(NLD_TRACE_ATTENTION, s);
             HIP_TRY(launch_attention(D, L.attn_kh, L.attn_z, L.units, at_, s));

@@ -1689,8 +1689,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
     const int nst = blockpart ? 1 : (kend > kbeg ? (kend - kbeg + 63) / 64 : 0);
     NLD_TS(TL_ATTENTION, 1);   // committed length known
     if (!blockpart) {
-        if (nst > 1) s1 = gload(kbeg + 64);
-        if (nst > 2) s2 = gload(kbeg + 128);
+        if (nst > 1 && a.late < 2) s1 = gload(kbeg + 64);
+        if (nst > 2 && a.late < 1) s2 = gload(kbeg + 128);
     }
 
     f32x4_t acc[DT];
@@ -1793,6 +1793,8 @@ __global__ void __launch_bounds__(512) attention_kernel(AttnArgs a) {
         // and st+2 are in flight in registers (s1 and s2 by turns; the loop is unrolled by
         // two so that no register copy waits on a load still in flight).
         if (nst > 0) lstore(s0, 0);
+        if (nst > 1 && a.late >= 2) s1 = gload(kbeg + 64);
+        if (nst > 2 && a.late >= 1) s2 = gload(kbeg + 128);
         __syncthreads();
         NLD_TS(TL_ATTENTION, 2);   // first stage in LDS
         for (int st = 0; st < nst; st += 2) {

@@ -194,6 +194,8 @@ struct AttnArgs {
     int items;
     int n_seq;           // sequences (units / n_kv_heads)
     uint32_t plain;      // PlainSite bits: SITE_P (probabilities), SITE_O (the merged output)
+    int late;            // prefix stages 1, 2 requested: 0 with the first, 1 stage 2 once the first is in
+                         // LDS, 2 both once the first is in LDS
 };
 
 struct EmbedArgs {
