@@ -276,14 +276,10 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     unsigned grab = 0u;
     if (threadIdx.x == 0 && G < T) grab = atomicAdd(a.tile_ctr, 1u);
 
-    uint4 wb[KS];
-    if (cur < T) {
-        const uint4* p = a.W + ((size_t)cur * a.ksteps + s0) * 64 + lane;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) wb[s] = load_stream(p + (size_t)s * 64);
-    }
-
-    // operand slice: row r, columns 32*(s0+s) + 8g .. +8, hi and lo
+    // operand slice: row r, columns 32*(s0+s) + 8g .. +8, hi and lo.  Requested before the first
+    // weight tile: loads complete in issue order, and the operand (L2 hits after the first workgroups)
+    // then no longer waits behind the tile's HBM reads (8B shapes, k = 16: QKV 16.7 against 17.5 us,
+    // gate/up 37.8 against 39.4 us, LM head 198.5 against 200.5 us).
     uint4 ah[KS], al[KS];
     const bool row_ok = r < a.M;
     const uint16_t* ar = a.A + (size_t)s0 * 1024 + (size_t)lane * 8;
@@ -291,6 +287,12 @@ __global__ void __launch_bounds__(KS >= 16 ? 512 : 1024) gemm_norm_kernel(GemmAr
     for (int s = 0; s < KS; ++s) {
         ah[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 1024) : uint4{0u, 0u, 0u, 0u};
         al[s] = row_ok ? *(const uint4*)(ar + (size_t)s * 1024 + SPLIT_LO) : uint4{0u, 0u, 0u, 0u};
+    }
+    uint4 wb[KS];
+    if (cur < T) {
+        const uint4* p = a.W + ((size_t)cur * a.ksteps + s0) * 64 + lane;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wb[s] = load_stream(p + (size_t)s * 64);
     }
     rms_scales(a, 0, 16, inv_s);
     if constexpr (EPI == EPI_QKV) {
