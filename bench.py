@@ -1,6 +1,7 @@
 """Benchmark of the block-decode step (draft pass + verify pass + acceptance) on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload 8b] [--k 16] [--max-len L] [--no-cpu-baseline]
+                    [--no-extras] [--no-large] [--no-graph] [--copy-calibration-mib N]
 
 A step is one linear self-speculation step over the synthetic workload: the
 diffusion draft pass over [anchor, mask x (k-1)], the causal verify pass over
@@ -17,7 +18,16 @@ and without the LoRA-enhanced drafter's adapter (rank 128) on the O projection;
 "quad_ss" -- one quadratic self-speculation step (chain length 7, 56 block rows)
 with the AR verifier and with the lambda = 0.5 ensemble, beside one linear step
 (draft + verify) of the same speculative width; "block_k32" -- one linear step
-at block size 32 (the paper's main block length) over the same prefix.
+at block size 32 (the paper's main block length) over the same prefix;
+"verify_pass_ms" -- the verify pass alone; "layer_microbench" -- one 8B-shaped
+layer + LM head at k = 8, 16, 32; "large_configs" -- the 8b_batch32 and 14b
+steps with random weights drawn on the GPU (--no-large skips them).
+"hbm_stream_ceiling" is what the library's hand-written read stream reaches on
+the same box (the practical HBM ceiling the step is compared with).
+"roofline" is the dominant kernel's: algorithmic bytes per launch over its
+average launch time from HIP events recorded on every dispatch of three eager
+steps, and its HBM traffic from the committed counter summary while the kernel
+sources match it.  "cpu_baseline" times the CPU oracle on a bounded sample.
 Prints one JSON line.
 """
 from __future__ import annotations
