@@ -474,6 +474,35 @@ def test_8b_layer_block_pass(R, layer8b, k, mode):
     assert R.read_device_status(ws) == 0
 
 
+@pytest.mark.parametrize("env", ["NLD_ATTN_LATE=0", "NLD_ATTN_LATE=1", "NLD_STREAM_NW_RESID=8"])
+def test_8b_layer_alternative_launch_paths(R, layer8b, monkeypatch, env):
+    """The launch paths kept selectable beside the defaults: a prefix split's stages 1 and 2 requested
+    together with stage 0 or stage 2 alone deferred, and the 16-row O projection on 8 wavefronts.
+    Each gives the same pass as the default within the fp32 rounding of its reductions, and is within
+    tolerance of the oracle, in both masks."""
+    t = layer8b
+    shape, k = t["shape"], 16
+    name, value = env.split("=")
+    tok = torch.from_numpy(synth_tokens(shape, t["seed"], "8b_layer.alt.block", (1, k))).cuda()
+    for mode in (O.VERIFY, O.DRAFT):
+        ref = O.block_forward(t["w"], t["okv"], tok.cpu().numpy(), mode)[0]
+        gm = R.VERIFY if mode == O.VERIFY else R.DRAFT
+        ws = R.Workspace(t["model"], 1, k, t["cache"].max_len)
+        monkeypatch.delenv(name, raising=False)
+        base = R.block_forward(t["model"], t["cache"], ws, tok, gm)[0].cpu().numpy()
+        monkeypatch.setenv(name, value)
+        alt = R.block_forward(t["model"], t["cache"], ws, tok, gm)[0].cpu().numpy()
+        monkeypatch.delenv(name, raising=False)
+        e = rel_err(alt, ref)
+        log("8b_layer k=16 %s %s: rel err %.3e, against the default path %.3e" % (mode, env, e, rel_err(alt, base)))
+        assert e <= TOL
+        if name == "NLD_ATTN_LATE":   # the same arithmetic in the same order: only when loads are issued
+            assert np.array_equal(alt, base)
+        else:
+            assert rel_err(alt, base) < 1e-4
+        assert R.read_device_status(ws) == 0
+
+
 @pytest.mark.parametrize("mode", [O.VERIFY, O.DRAFT])
 def test_8b_layer_long_cache_block_pass(R, layer8b, mode):
     """A cache whose capacity (16384) is eight times its committed prefix (2048): one sequence's prefix
