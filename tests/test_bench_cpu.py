@@ -32,8 +32,6 @@ def test_pass_bytes_are_weights_kv_and_small_activations():
     kv = s.n_layers * 2 * 2 * int(np.sum(plens + k)) * s.kv_dim
     rest = total - s.weight_bytes() - kv
     assert 0 < rest < 0.01 * total
-    # the step moves two passes
-    assert 2 * total == 2 * bench.pass_bytes(s, 1, k, plens)
 
 
 def test_measured_traffic_follows_the_kernel_sources(monkeypatch):
